@@ -1,0 +1,57 @@
+"""Exact bfloat16 codec for the oracle (test infrastructure only).
+
+bfloat16 keeps the float32 sign and 8-bit exponent and 7 stored significand
+bits.  The paper does not state the cache dtype; the stored cache is taken to
+be bfloat16 with round-to-nearest-even (ties to even) for the Qwen-shaped
+workloads.  Values are carried as uint16 bit patterns because numpy has no
+bfloat16 type.
+
+``encode`` rounds a float64 value to bfloat16 in ONE step (no detour through
+float32, which would round twice).
+"""
+import numpy as np
+
+_EXP_MIN = -126          # smallest normal exponent of bfloat16 (same as float32)
+_MANT_BITS = 7           # stored significand bits
+
+
+def decode(bits):
+    """uint16 bf16 bit patterns -> float64 (exact)."""
+    b = np.asarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def encode(x):
+    """float64 -> uint16 bf16 bit patterns, round to nearest, ties to even.
+
+    For |x| with leading-bit exponent e the representable spacing (quantum) is
+    2**(e - 7) for normals and 2**(-126 - 7) in the subnormal range.  x/quantum
+    is exact (power-of-two scaling), numpy.rint rounds half to even, and the
+    rounded value times the quantum is exactly representable in bf16 (and in
+    float32), so its float32 bit pattern shifted right by 16 is the answer.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    sign = np.where(np.signbit(x), np.uint16(0x8000), np.uint16(0))
+    a = np.abs(x)
+    out = np.zeros(x.shape, dtype=np.uint16)
+    finite = np.isfinite(a)
+    nz = finite & (a > 0)
+    if np.any(nz):
+        an = a[nz]
+        _, ex = np.frexp(an)                  # an = m * 2**ex, m in [0.5, 1)
+        lead = ex.astype(np.int64) - 1        # exponent of the leading bit
+        qexp = np.maximum(lead, _EXP_MIN) - _MANT_BITS
+        y = np.ldexp(np.rint(np.ldexp(an, -qexp)), qexp)
+        ovf = y >= 2.0 ** 128
+        y32 = np.where(ovf, np.float32(0), y).astype(np.float32)
+        hb = (y32.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+        hb = np.where(ovf, np.uint16(0x7F80), hb)
+        out[nz] = hb
+    out[np.isinf(a)] = np.uint16(0x7F80)
+    out[np.isnan(a)] = np.uint16(0x7FC0)
+    return out | sign
+
+
+def round_f64(x):
+    """float64 -> float64 value of its bf16 rounding."""
+    return decode(encode(x))
