@@ -1,0 +1,203 @@
+/*
+ * chronostitch.h -- C ABI of the ChronoStitch KV-composition hot path for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The method (ChronoStitch, Section 2) composes independently prefilled
+ * visual KV caches: stored post-rotary keys are moved from local chunk
+ * coordinates to a global three-axis (t, h, w) mRoPE timeline by a delta
+ * rotation (Eq. 3); later-chunk tokens are ranked by the deviation of their
+ * recomputed scoring-layer key (Eq. 5); the top rho fraction is recomputed,
+ * attending causally over the composed cache (Eq. 1), and their fresh keys
+ * and values are scattered back.
+ *
+ * Conventions shared by every entry point
+ *  - All functions are extern "C", take plain pointers and sizes, and never
+ *    throw.  They return CS_OK or an error code; cs_last_error() then gives
+ *    a human-readable message (thread-local, valid until the next call on
+ *    the same thread).
+ *  - Argument errors are detected before anything is enqueued and before any
+ *    HIP runtime call, so a rejected call leaves device memory untouched.
+ *  - DEVICE pointers are device memory of the current HIP device; HOST
+ *    pointers are read (or written) before the call returns.  The caller
+ *    owns every buffer; the library allocates no device memory.  Scratch
+ *    memory is a caller-provided workspace sized by the *_workspace query.
+ *  - Device work is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream).  Outputs in device memory are valid once the stream has
+ *    reached the enqueued work.  Host outputs are written synchronously.
+ *  - Calls are re-entrant for distinct buffers and streams.  Inputs must not
+ *    alias outputs except for the documented in-place caches.
+ *  - Tensor layouts are dense, row-major, with the last index contiguous:
+ *      caches      [L][H_kv][T][D]   chunks are contiguous token ranges, so
+ *                                    the concatenation of the chunk caches is
+ *                                    the layout itself
+ *      fresh Q     [L][H_q][n][D]    row r <-> token chunk_start[1] + r
+ *      fresh K, V  [L][H_kv][n][D]   row r <-> token chunk_start[1] + r
+ *    where n = T - chunk_start[1] is the number of later-chunk tokens.
+ *  - Element type of every K/V/Q/O tensor is geometry.dtype; bf16 values are
+ *    rounded to nearest even.
+ */
+#ifndef CHRONOSTITCH_H
+#define CHRONOSTITCH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CS_OK = 0,
+  CS_ERR_INVALID_ARGUMENT = 1,   /* a pointer, size or value is out of its documented range */
+  CS_ERR_UNSUPPORTED = 2,        /* a valid request this build does not implement             */
+  CS_ERR_WORKSPACE_TOO_SMALL = 3,/* workspace_bytes is below the *_workspace query's answer    */
+  CS_ERR_HIP = 4                 /* a HIP runtime call or kernel launch failed                 */
+} cs_status;
+
+typedef enum { CS_F32 = 0, CS_BF16 = 1 } cs_dtype;
+
+/* Geometry of a composed cache (Section 3 gives the model's: 36 layers,
+ * 16 query heads, 2 KV heads, head dim 128, mRoPE sections 16/24/24).
+ *   n_q_heads % n_kv_heads == 0; query head h reads KV head h / (n_q_heads/n_kv_heads).
+ *   head_dim even, 2 <= head_dim <= 512.
+ *   sections: rotary pairs on the t, h, w axes, in that order; they sum to
+ *     head_dim/2.  Pair i is the element pair (i, i + head_dim/2) and rotates
+ *     with axis t for i < s_t, h for i < s_t + s_h, w otherwise (Eq. 2).
+ *   rope_base: theta_i = rope_base^(-2i/head_dim) when inv_freq is NULL.
+ *   inv_freq: HOST [head_dim/2] float64 theta_i overriding rope_base, or NULL.
+ *   chunk_start: HOST [n_chunks + 1], 0 = s_0 < s_1 < ... < s_N = n_tokens;
+ *     chunk c owns tokens [s_c, s_{c+1}).  n_tokens < 2^31.             */
+typedef struct {
+  int32_t n_layers;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t sections[3];
+  int32_t dtype;               /* cs_dtype */
+  double rope_base;
+  const double* inv_freq;
+  int64_t n_tokens;
+  int32_t n_chunks;
+  const int64_t* chunk_start;
+} cs_geometry;
+
+/* ---------------------------------------------------------------------------
+ * compose_rebase_k -- Section 2, Eq. 3 (three-axis delta rotation).
+ *
+ * Gives chunk c the global coordinates p' = p + Delta_c and rotates every
+ * stored post-rotary key of the chunk, in place, by R(Delta): pair i turns by
+ * Delta_c[sigma(i)] * theta_i, so a key stored as f(x, p) becomes f(x, p').
+ * Angles are formed in float64 and reduced modulo 2*pi before the cos/sin
+ * table is rounded to float32, so offsets of 1e5 and beyond stay accurate.
+ * Chunks with Delta_c = (0,0,0) are not touched (bit-identical).  Values are
+ * never rotated, so there is no V argument.
+ *
+ *   g             geometry (HOST)
+ *   k_cache       DEVICE [L][H_kv][T][D] keys, post-rotary at local
+ *                 coordinates on entry and at global coordinates on return
+ *   chunk_offsets HOST int32 [n_chunks][3]: (dt, dh, dw) = p' - p of chunk c
+ *   local_coords  HOST int32 [T][3] token coordinates (t, h, w), or NULL
+ *   global_coords HOST int32 [T][3] output p' = p + Delta_c, or NULL; needs
+ *                 local_coords.  Written before the call returns.
+ *   stream        hipStream_t or NULL
+ * Errors: CS_ERR_INVALID_ARGUMENT for a bad geometry, a NULL k_cache or
+ * chunk_offsets, or global_coords without local_coords.                    */
+cs_status compose_rebase_k(const cs_geometry* g, void* k_cache,
+                           const int32_t* chunk_offsets,
+                           const int32_t* local_coords, int32_t* global_coords,
+                           void* stream);
+
+/* ---------------------------------------------------------------------------
+ * score_deviation_topk -- Section 2, Eq. 5 and the top-rho selection after it.
+ *
+ * For every later-chunk token t in [s_1, T):
+ *   delta_t = || k_fresh[:, t - s_1, :] - k_cache[score_layer][:, t, :] ||_2
+ * over all H_kv x D elements, accumulated in float64 and rounded once to
+ * float32.  Then selects the k = n_select(rho, n) largest float32 scores,
+ * lower token index first among equal scores, and writes their token indices
+ * in ascending order.  n_select(rho, n) = 0 if rho == 0, else
+ * min(n, ceil(rho * n - 1e-9)).
+ *
+ *   g             geometry (HOST)
+ *   k_cache       DEVICE [L][H_kv][T][D] keys, already re-based
+ *   score_layer   layer whose keys are compared, 0 <= score_layer < L (the
+ *                 paper scores layer 1)
+ *   k_fresh       DEVICE [H_kv][n][D] recomputed keys at score_layer,
+ *                 post-rotary at global coordinates
+ *   rho           repair fraction in [0, 1]
+ *   scores        DEVICE float32 [n] output delta_t, or NULL (then the
+ *                 workspace holds them)
+ *   sel_idx       DEVICE int32 [k] output, ascending token indices in [s_1, T);
+ *                 may be NULL when k == 0
+ *   n_sel         HOST int64 output k (computed on the host; no device sync)
+ *   workspace     DEVICE scratch of workspace_bytes, >= the query's answer
+ * Errors: CS_ERR_INVALID_ARGUMENT (bad geometry, rho outside [0,1] or NaN,
+ * score_layer out of range, NULL required pointer), CS_ERR_WORKSPACE_TOO_SMALL.
+ * Scores must be finite (NaN ranking is undefined).                       */
+cs_status score_deviation_topk_workspace(const cs_geometry* g, size_t* bytes);
+cs_status score_deviation_topk(const cs_geometry* g, const void* k_cache,
+                               int32_t score_layer, const void* k_fresh,
+                               double rho, float* scores, int32_t* sel_idx,
+                               int64_t* n_sel, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * selective_attend_scatter -- Section 2, Eq. 1 and the repair step.
+ *
+ * For each layer l in [layer_begin, layer_end):
+ *   1. scatter: k_cache[l][h][sel_idx[m]] <- k_fresh[l][h][sel_idx[m] - s_1]
+ *      and the same for V; every other row is unchanged.
+ *   2. attend: for slot m (token t = sel_idx[m]) and query head h
+ *      (KV head kv = h / (H_q/H_kv)), with q = q_fresh[l][h][t - s_1],
+ *        out[l][h][m] = softmax_j(q . K[l][kv][j] / sqrt(D)) V[l][kv][j],
+ *      j = 0 .. t (causal in cache order, self included), over the
+ *      post-scatter cache.  Softmax and accumulation run in float32.
+ *      lse[l][h][m] = log(sum_j exp(q . K[l][kv][j] / sqrt(D))).
+ * Layers are independent, so one call over many layers equals one call per
+ * layer; per-layer calls mirror the model's layer-by-layer recompute.
+ *
+ *   g              geometry (HOST)
+ *   k_cache,v_cache DEVICE [L][H_kv][T][D], rows sel_idx overwritten in place
+ *   layer_begin, layer_end  0 <= begin <= end <= L
+ *   sel_idx        DEVICE int32 [n_sel], strictly ascending, in [s_1, T)
+ *                  (as written by score_deviation_topk; not checked)
+ *   n_sel          0 <= n_sel <= n
+ *   q_fresh        DEVICE [L][H_q][n][D] fresh queries (post-rotary, global)
+ *   k_fresh,v_fresh DEVICE [L][H_kv][n][D] fresh keys / values
+ *   out            DEVICE [L][H_q][n_sel][D] output, slot order of sel_idx
+ *   lse            DEVICE float32 [L][H_q][n_sel] output, or NULL
+ *   workspace      DEVICE scratch, >= selective_attend_scatter_workspace()
+ *                  for the same n_sel and layer count
+ * Errors: CS_ERR_INVALID_ARGUMENT, CS_ERR_WORKSPACE_TOO_SMALL, CS_ERR_HIP. */
+cs_status selective_attend_scatter_workspace(const cs_geometry* g, int64_t n_sel,
+                                             int32_t n_layers_per_call,
+                                             size_t* bytes);
+cs_status selective_attend_scatter(const cs_geometry* g, void* k_cache,
+                                   void* v_cache, int32_t layer_begin,
+                                   int32_t layer_end, const int32_t* sel_idx,
+                                   int64_t n_sel, const void* q_fresh,
+                                   const void* k_fresh, const void* v_fresh,
+                                   void* out, float* lse, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+/* Thread-local text describing the last non-OK status on this thread. */
+const char* cs_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * Kernel tracing (measurement aid, off by default).
+ * While enabled, every kernel the library launches is bracketed by a pair of
+ * hipEvents on its own stream.  cs_trace_collect() synchronises those events
+ * and accumulates, per kernel name, the number of launches and their total
+ * duration.  Not thread-safe: trace from one thread at a time.             */
+cs_status cs_trace_enable(int32_t on);
+cs_status cs_trace_collect(void);
+int32_t cs_trace_count(void);
+cs_status cs_trace_get(int32_t i, const char** name, int64_t* launches,
+                       double* total_ms);
+void cs_trace_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CHRONOSTITCH_H */

@@ -25,31 +25,27 @@ def encode(x):
     """float64 -> uint16 bf16 bit patterns, round to nearest, ties to even.
 
     For |x| with leading-bit exponent e the representable spacing (quantum) is
-    2**(e - 7) for normals and 2**(-126 - 7) in the subnormal range.  x/quantum
-    is exact (power-of-two scaling), numpy.rint rounds half to even, and the
-    rounded value times the quantum is exactly representable in bf16 (and in
-    float32), so its float32 bit pattern shifted right by 16 is the answer.
+    2**(e - 7) for normals and 2**(-126 - 7) in the subnormal range.  Scaling
+    by the inverse quantum is exact (a power of two), numpy.rint rounds half
+    to even, and the rounded value times the quantum is exactly representable
+    in bf16 (and in float32), so its float32 bit pattern shifted right by 16
+    is the answer.  The exponent e is read from the float64 bit pattern.
     """
     x = np.asarray(x, dtype=np.float64)
-    sign = np.where(np.signbit(x), np.uint16(0x8000), np.uint16(0))
     a = np.abs(x)
-    out = np.zeros(x.shape, dtype=np.uint16)
-    finite = np.isfinite(a)
-    nz = finite & (a > 0)
-    if np.any(nz):
-        an = a[nz]
-        _, ex = np.frexp(an)                  # an = m * 2**ex, m in [0.5, 1)
-        lead = ex.astype(np.int64) - 1        # exponent of the leading bit
-        qexp = np.maximum(lead, _EXP_MIN) - _MANT_BITS
-        y = np.ldexp(np.rint(np.ldexp(an, -qexp)), qexp)
-        ovf = y >= 2.0 ** 128
-        y32 = np.where(ovf, np.float32(0), y).astype(np.float32)
-        hb = (y32.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
-        hb = np.where(ovf, np.uint16(0x7F80), hb)
-        out[nz] = hb
-    out[np.isinf(a)] = np.uint16(0x7F80)
-    out[np.isnan(a)] = np.uint16(0x7FC0)
-    return out | sign
+    ebits = (a.view(np.uint64) >> np.uint64(52)).astype(np.int64)   # biased exponent
+    lead = np.where(ebits == 0, -1075, ebits - 1023)                 # fp64 subnormals: far below bf16 range
+    qexp = np.maximum(lead, _EXP_MIN) - _MANT_BITS
+    q = ((qexp + 1023).astype(np.uint64) << np.uint64(52)).view(np.float64)       # 2**qexp
+    iq = ((1023 - qexp).astype(np.uint64) << np.uint64(52)).view(np.float64)      # 2**-qexp
+    with np.errstate(over="ignore", invalid="ignore"):
+        y = np.rint(a * iq) * q
+        ovf = ~(y < 2.0 ** 128)                                      # overflow, inf and nan
+        hb = (np.where(ovf, 0.0, y).astype(np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+    hb = np.where(ovf, np.uint16(0x7F80), hb)
+    hb = np.where(np.isnan(x), np.uint16(0x7FC0), hb)
+    sign = np.where(np.signbit(x), np.uint16(0x8000), np.uint16(0))
+    return (hb | sign).astype(np.uint16)
 
 
 def round_f64(x):

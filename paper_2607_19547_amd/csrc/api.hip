@@ -1,0 +1,281 @@
+// C-ABI entry points: argument validation, host-side coordinate shift,
+// workspace sizing, kernel tracing and error reporting.
+#include <math.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "cs_common.h"
+
+namespace cs {
+
+static thread_local std::string t_error;
+
+void set_error(const std::string& msg) { t_error = msg; }
+
+cs_status fail(cs_status code, const std::string& msg) {
+  t_error = msg;
+  return code;
+}
+
+cs_status check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess)
+    return fail(CS_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  return CS_OK;
+}
+
+// ------------------------------------------------------------------ tracing
+namespace {
+struct Pending {
+  std::string name;
+  hipEvent_t a, b;
+};
+struct Acc {
+  int64_t launches = 0;
+  double ms = 0.0;
+};
+bool g_trace_on = false;
+std::vector<Pending> g_pending;
+std::vector<std::pair<std::string, Acc>> g_acc;
+std::vector<hipEvent_t> g_pool;
+
+hipEvent_t take_event() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+}  // namespace
+
+TraceScope::TraceScope(const char* n, hipStream_t s) : name(n), stream(s), slot(-1) {
+  if (!g_trace_on) return;
+  hipEvent_t a = take_event(), b = take_event();
+  if (!a || !b) return;
+  hipEventRecord(a, s);
+  g_pending.push_back({name, a, b});
+  slot = (int)g_pending.size() - 1;
+}
+
+TraceScope::~TraceScope() {
+  if (slot >= 0) hipEventRecord(g_pending[slot].b, stream);
+}
+
+// ------------------------------------------------------------------ geometry
+cs_status check_geometry(const cs_geometry* g, Geo* o) {
+  if (!g) return fail(CS_ERR_INVALID_ARGUMENT, "geometry is NULL");
+  if (g->n_layers < 1) return fail(CS_ERR_INVALID_ARGUMENT, "n_layers must be >= 1");
+  if (g->n_q_heads < 1 || g->n_kv_heads < 1)
+    return fail(CS_ERR_INVALID_ARGUMENT, "head counts must be >= 1");
+  if (g->n_q_heads % g->n_kv_heads)
+    return fail(CS_ERR_INVALID_ARGUMENT, "n_q_heads must be a multiple of n_kv_heads");
+  if (g->head_dim < 2 || g->head_dim > 512 || (g->head_dim & 1))
+    return fail(CS_ERR_INVALID_ARGUMENT, "head_dim must be even and in [2, 512]");
+  if (g->sections[0] < 0 || g->sections[1] < 0 || g->sections[2] < 0 ||
+      (int64_t)g->sections[0] + g->sections[1] + g->sections[2] != g->head_dim / 2)
+    return fail(CS_ERR_INVALID_ARGUMENT, "sections must be >= 0 and sum to head_dim/2");
+  if (g->dtype != CS_F32 && g->dtype != CS_BF16)
+    return fail(CS_ERR_INVALID_ARGUMENT, "dtype must be CS_F32 or CS_BF16");
+  if (!g->inv_freq && !(g->rope_base > 0.0 && isfinite(g->rope_base)))
+    return fail(CS_ERR_INVALID_ARGUMENT, "rope_base must be finite and > 0 when inv_freq is NULL");
+  if (g->n_tokens < 1 || g->n_tokens >= (int64_t(1) << 31))
+    return fail(CS_ERR_INVALID_ARGUMENT, "n_tokens must be in [1, 2^31)");
+  if (g->n_chunks < 1) return fail(CS_ERR_INVALID_ARGUMENT, "n_chunks must be >= 1");
+  if (!g->chunk_start) return fail(CS_ERR_INVALID_ARGUMENT, "chunk_start is NULL");
+  if (g->chunk_start[0] != 0) return fail(CS_ERR_INVALID_ARGUMENT, "chunk_start[0] must be 0");
+  for (int c = 0; c < g->n_chunks; ++c)
+    if (g->chunk_start[c + 1] <= g->chunk_start[c])
+      return fail(CS_ERR_INVALID_ARGUMENT, "chunk_start must be strictly increasing");
+  if (g->chunk_start[g->n_chunks] != g->n_tokens)
+    return fail(CS_ERR_INVALID_ARGUMENT, "chunk_start[n_chunks] must equal n_tokens");
+  o->L = g->n_layers;
+  o->Hq = g->n_q_heads;
+  o->Hkv = g->n_kv_heads;
+  o->G = g->n_q_heads / g->n_kv_heads;
+  o->D = g->head_dim;
+  o->P = g->head_dim / 2;
+  for (int i = 0; i < 3; ++i) o->sec[i] = g->sections[i];
+  o->dtype = g->dtype;
+  o->esize = g->dtype == CS_BF16 ? 2 : 4;
+  o->T = g->n_tokens;
+  o->N = g->n_chunks;
+  o->cs = g->chunk_start;
+  o->cs1 = g->n_chunks >= 2 ? g->chunk_start[1] : g->n_tokens;
+  o->n = o->T - o->cs1;
+  return CS_OK;
+}
+
+int64_t n_select(double rho, int64_t n) {
+  if (rho == 0.0 || n == 0) return 0;
+  int64_t k = (int64_t)ceil(rho * (double)n - 1e-9);
+  if (k < 0) k = 0;
+  return k > n ? n : k;
+}
+
+static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace cs
+
+using namespace cs;
+
+// ====================================================================== exports
+extern "C" {
+
+const char* cs_last_error(void) { return t_error.c_str(); }
+
+cs_status compose_rebase_k(const cs_geometry* gp, void* k_cache, const int32_t* chunk_offsets,
+                           const int32_t* local_coords, int32_t* global_coords, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  if (!k_cache) return fail(CS_ERR_INVALID_ARGUMENT, "k_cache is NULL");
+  if (!chunk_offsets) return fail(CS_ERR_INVALID_ARGUMENT, "chunk_offsets is NULL");
+  if (global_coords && !local_coords)
+    return fail(CS_ERR_INVALID_ARGUMENT, "global_coords needs local_coords");
+  // Coordinate shift (host): p' = p + Delta_c for every token of chunk c.
+  if (global_coords) {
+    for (int c = 0; c < g.N; ++c)
+      for (int64_t t = g.cs[c]; t < g.cs[c + 1]; ++t)
+        for (int a = 0; a < 3; ++a)
+          global_coords[3 * t + a] = local_coords[3 * t + a] + chunk_offsets[3 * c + a];
+  }
+  // theta_i in float64 (host): the caller's table or base^(-2i/D).
+  std::vector<double> theta(g.P);
+  for (int i = 0; i < g.P; ++i)
+    theta[i] = gp->inv_freq ? gp->inv_freq[i] : pow(gp->rope_base, -2.0 * i / (double)g.D);
+  for (int i = 0; i < g.P; ++i)
+    if (!isfinite(theta[i])) return fail(CS_ERR_INVALID_ARGUMENT, "inv_freq holds a non-finite value");
+  return launch_rebase(g, k_cache, chunk_offsets, theta.data(), (hipStream_t)stream);
+}
+
+cs_status score_deviation_topk_workspace(const cs_geometry* gp, size_t* bytes) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  if (!bytes) return fail(CS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  *bytes = align_up((size_t)g.n * sizeof(float), 256);
+  return CS_OK;
+}
+
+cs_status score_deviation_topk(const cs_geometry* gp, const void* k_cache, int32_t score_layer,
+                               const void* k_fresh, double rho, float* scores, int32_t* sel_idx,
+                               int64_t* n_sel, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  if (!n_sel) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel is NULL");
+  if (!(rho >= 0.0 && rho <= 1.0)) return fail(CS_ERR_INVALID_ARGUMENT, "rho must lie in [0, 1]");
+  if (score_layer < 0 || score_layer >= g.L)
+    return fail(CS_ERR_INVALID_ARGUMENT, "score_layer out of range");
+  int64_t k = n_select(rho, g.n);
+  if (g.n > 0) {
+    if (!k_cache || !k_fresh) return fail(CS_ERR_INVALID_ARGUMENT, "k_cache or k_fresh is NULL");
+    if (k > 0 && !sel_idx) return fail(CS_ERR_INVALID_ARGUMENT, "sel_idx is NULL");
+    if (!scores) {
+      size_t need = align_up((size_t)g.n * sizeof(float), 256);
+      if (!workspace || workspace_bytes < need)
+        return fail(CS_ERR_WORKSPACE_TOO_SMALL, "workspace must hold n float32 scores when scores is NULL");
+      scores = (float*)workspace;
+    }
+  }
+  *n_sel = k;
+  if (g.n == 0) return CS_OK;
+  const char* kl = (const char*)k_cache + (size_t)score_layer * g.Hkv * g.T * g.D * g.esize;
+  return launch_score_select(g, kl, k_fresh, scores, sel_idx, k, (hipStream_t)stream);
+}
+
+cs_status selective_attend_scatter_workspace(const cs_geometry* gp, int64_t n_sel,
+                                             int32_t n_layers_per_call, size_t* bytes) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  if (!bytes) return fail(CS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  if (n_sel < 0 || n_sel > g.n) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel must be in [0, n]");
+  if (n_layers_per_call < 0 || n_layers_per_call > g.L)
+    return fail(CS_ERR_INVALID_ARGUMENT, "n_layers_per_call must be in [0, n_layers]");
+  AttnPlan p = plan_attention(g, n_sel);
+  *bytes = p.ws_bytes_per_layer * (size_t)n_layers_per_call;
+  return CS_OK;
+}
+
+cs_status selective_attend_scatter(const cs_geometry* gp, void* k_cache, void* v_cache,
+                                   int32_t layer_begin, int32_t layer_end, const int32_t* sel_idx,
+                                   int64_t n_sel, const void* q_fresh, const void* k_fresh,
+                                   const void* v_fresh, void* out, float* lse, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  if (layer_begin < 0 || layer_end < layer_begin || layer_end > g.L)
+    return fail(CS_ERR_INVALID_ARGUMENT, "need 0 <= layer_begin <= layer_end <= n_layers");
+  if (n_sel < 0 || n_sel > g.n) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel must be in [0, n]");
+  if (n_sel == 0 || layer_end == layer_begin) return CS_OK;
+  if (!k_cache || !v_cache || !sel_idx || !q_fresh || !k_fresh || !v_fresh || !out)
+    return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  AttnPlan p = plan_attention(g, n_sel);
+  size_t need = p.ws_bytes_per_layer * (size_t)(layer_end - layer_begin);
+  if (need && (!workspace || workspace_bytes < need))
+    return fail(CS_ERR_WORKSPACE_TOO_SMALL,
+                "workspace smaller than selective_attend_scatter_workspace() (" + std::to_string(need) +
+                    " bytes)");
+  hipStream_t s = (hipStream_t)stream;
+  st = launch_scatter(g, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, k_fresh, v_fresh, s);
+  if (st) return st;
+  return launch_attention(g, p, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_fresh,
+                          out, lse, workspace, s);
+}
+
+// ------------------------------------------------------------------ tracing exports
+cs_status cs_trace_enable(int32_t on) {
+  g_trace_on = on != 0;
+  return CS_OK;
+}
+
+cs_status cs_trace_collect(void) {
+  for (auto& p : g_pending) {
+    if (hipEventSynchronize(p.b) != hipSuccess) return fail(CS_ERR_HIP, "hipEventSynchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) != hipSuccess)
+      return fail(CS_ERR_HIP, "hipEventElapsedTime failed");
+    bool found = false;
+    for (auto& kv : g_acc)
+      if (kv.first == p.name) {
+        kv.second.launches += 1;
+        kv.second.ms += ms;
+        found = true;
+        break;
+      }
+    if (!found) {
+      Acc a;
+      a.launches = 1;
+      a.ms = ms;
+      g_acc.push_back({p.name, a});
+    }
+    g_pool.push_back(p.a);
+    g_pool.push_back(p.b);
+  }
+  g_pending.clear();
+  return CS_OK;
+}
+
+int32_t cs_trace_count(void) { return (int32_t)g_acc.size(); }
+
+cs_status cs_trace_get(int32_t i, const char** name, int64_t* launches, double* total_ms) {
+  if (i < 0 || i >= (int32_t)g_acc.size()) return fail(CS_ERR_INVALID_ARGUMENT, "trace index out of range");
+  if (name) *name = g_acc[i].first.c_str();
+  if (launches) *launches = g_acc[i].second.launches;
+  if (total_ms) *total_ms = g_acc[i].second.ms;
+  return CS_OK;
+}
+
+void cs_trace_reset(void) { g_acc.clear(); }
+
+}  // extern "C"

@@ -1,0 +1,598 @@
+// Scatter of fresh K/V rows and causal GQA attention of the selected rows
+// (Eq. 1 and the repair step of Section 2).
+//
+// MFMA path (bf16, head_dim 128, G = H_q/H_kv dividing 32)
+// ---------------------------------------------------------
+// A workgroup owns one KV head, a tile of consecutive selection slots and one
+// key split.  Its 4 wavefronts each hold 32 query vectors: 32/G selected rows
+// x the G query heads that share the KV head, so every K/V tile staged in LDS
+// serves 128 query vectors.  Per 64-key tile a wavefront computes
+//   S^T = K Q^T         (v_mfma_f32_32x32x16_bf16, K from LDS, Q in VGPRs)
+// so each lane ends up holding 32 scores of ONE query; the softmax runs on
+// those registers (exp2 with the 1/sqrt(D) and log2(e) factors folded into one
+// FMA, a lazy running max that rescales only when the max grows by > 2^8),
+// and the probabilities are packed to bf16 directly as the B operand of
+//   O^T += V^T P^T      (V^T from LDS, stored transposed with the key order
+//                        permuted to match the accumulator layout of S^T).
+// K/V tiles are double-buffered in LDS and prefetched into VGPRs one tile
+// ahead.  Rows are causal in cache order: key j is visible to row t iff
+// j <= t; tiles below every row's limit skip the mask.  Long rows are split
+// over the key axis; partial (O, max, sum) go to the workspace and a combine
+// kernel merges them.  Tiles are issued longest first.
+//
+// Generic path: one wavefront per (row, query head), float32 arithmetic, any
+// head_dim <= 512 and either storage dtype.
+#include <math.h>
+
+#include <algorithm>
+
+#include "cs_common.h"
+
+namespace cs {
+
+// ============================================================== scatter
+__global__ __launch_bounds__(256) void scatter_rows(char* __restrict__ k, char* __restrict__ v,
+                                                    const char* __restrict__ kf,
+                                                    const char* __restrict__ vf,
+                                                    const int32_t* __restrict__ sel, int64_t n_sel,
+                                                    int64_t T, int64_t n, int64_t cs1, int Hkv,
+                                                    int row_bytes, int lb) {
+  const int layer = lb + blockIdx.y;
+  const int words = row_bytes / 16;
+  const int64_t total = (int64_t)Hkv * n_sel * words;
+  for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < total;
+       w += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(w % words);
+    const int64_t hm = w / words;
+    const int64_t m = hm % n_sel;
+    const int h = (int)(hm / n_sel);
+    const int64_t t = sel[m];
+    if (t < cs1 || t >= T) continue;  // out-of-contract index: never write outside the cache
+    const int64_t dst = (((int64_t)layer * Hkv + h) * T + t) * row_bytes + 16 * c;
+    const int64_t src = (((int64_t)layer * Hkv + h) * n + (t - cs1)) * row_bytes + 16 * c;
+    *(u32x4*)(k + dst) = *(const u32x4*)(kf + src);
+    *(u32x4*)(v + dst) = *(const u32x4*)(vf + src);
+  }
+}
+
+__global__ __launch_bounds__(256) void scatter_rows_w4(char* __restrict__ k, char* __restrict__ v,
+                                                       const char* __restrict__ kf,
+                                                       const char* __restrict__ vf,
+                                                       const int32_t* __restrict__ sel, int64_t n_sel,
+                                                       int64_t T, int64_t n, int64_t cs1, int Hkv,
+                                                       int row_bytes, int lb) {
+  const int layer = lb + blockIdx.y;
+  const int words = row_bytes / 4;
+  const int64_t total = (int64_t)Hkv * n_sel * words;
+  for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < total;
+       w += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(w % words);
+    const int64_t hm = w / words;
+    const int64_t m = hm % n_sel;
+    const int h = (int)(hm / n_sel);
+    const int64_t t = sel[m];
+    if (t < cs1 || t >= T) continue;
+    const int64_t dst = (((int64_t)layer * Hkv + h) * T + t) * row_bytes + 4 * c;
+    const int64_t src = (((int64_t)layer * Hkv + h) * n + (t - cs1)) * row_bytes + 4 * c;
+    *(uint32_t*)(k + dst) = *(const uint32_t*)(kf + src);
+    *(uint32_t*)(v + dst) = *(const uint32_t*)(vf + src);
+  }
+}
+
+cs_status launch_scatter(const Geo& g, void* k, void* v, int lb, int le, const int32_t* sel,
+                         int64_t n_sel, const void* kf, const void* vf, hipStream_t s) {
+  const int row_bytes = g.D * g.esize;
+  const bool wide = row_bytes % 16 == 0;
+  const int64_t total = (int64_t)g.Hkv * n_sel * (wide ? row_bytes / 16 : row_bytes / 4);
+  const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 65535);
+  TraceScope tr("scatter_rows", s);
+  if (wide)
+    hipLaunchKernelGGL(scatter_rows, dim3(blocks, le - lb), dim3(256), 0, s, (char*)k, (char*)v,
+                       (const char*)kf, (const char*)vf, sel, n_sel, g.T, g.n, g.cs1, g.Hkv, row_bytes, lb);
+  else
+    hipLaunchKernelGGL(scatter_rows_w4, dim3(blocks, le - lb), dim3(256), 0, s, (char*)k, (char*)v,
+                       (const char*)kf, (const char*)vf, sel, n_sel, g.T, g.n, g.cs1, g.Hkv, row_bytes, lb);
+  return check_launch("scatter launch");
+}
+
+// ============================================================== MFMA attention
+constexpr int kKT = 64;       // keys per tile
+constexpr int kKPitch = 136;  // LDS row pitch of K, bf16 elements (128 + 8)
+constexpr int kVPitch = 72;   // LDS row pitch of V^T, bf16 elements (64 + 8)
+constexpr int kQPerWG = 128;  // query vectors per workgroup
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr float kRescaleLog2 = 8.0f;  // lazy rescale threshold (max growth 2^8)
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* sel;
+  uint16_t* out;
+  float* lse;
+  float* part;     // [layers in call][items][128][128] partial O (unnormalised)
+  float* part_ml;  // [layers in call][items][128][2] running max (log2 units), sum
+  int64_t T, n, n_sel, n_tiles;
+  int cs1, Hq, Hkv, lb;
+  int split, max_splits;
+  float scale_log2;  // log2(e) / sqrt(D)
+};
+
+// Lanes l and l^32 hold the same query: combine their values.
+__device__ __forceinline__ float pair_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Position of key j (0..63) inside a V^T row: within each 16-key group the
+// keys a lane half contributes to one MFMA k-step sit next to each other.
+__device__ __forceinline__ int vt_pos_of_quad(int kq) {
+  return 16 * (kq >> 2) + 8 * (kq & 1) + 4 * ((kq >> 1) & 1);
+}
+
+__device__ __forceinline__ uint32_t half_of(uint32_t w, int hi) { return hi ? (w >> 16) : (w & 0xffffu); }
+
+struct TileRegs {
+  u32x4 k[4];
+  u32x4 v[4];
+};
+
+__device__ __forceinline__ void load_tile(TileRegs& r, const uint16_t* kb, const uint16_t* vb, int kt,
+                                          int64_t T, int tid) {
+  const int c = tid & 15, rr = tid >> 4;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int key = kt + rr + 16 * j;
+    r.k[j] = key < T ? *(const u32x4*)(kb + (int64_t)key * 128 + 8 * c) : u32x4{0, 0, 0, 0};
+  }
+  const int kq = tid & 15, dc = tid >> 4;
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const int key = kt + 4 * kq + a;
+    r.v[a] = key < T ? *(const u32x4*)(vb + (int64_t)key * 128 + 8 * dc) : u32x4{0, 0, 0, 0};
+  }
+}
+
+__device__ __forceinline__ void store_tile(const TileRegs& r, uint16_t* Ks, uint16_t* Vt, int tid) {
+  const int c = tid & 15, rr = tid >> 4;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) *(u32x4*)(Ks + (rr + 16 * j) * kKPitch + 8 * c) = r.k[j];
+  const int kq = tid & 15, dc = tid >> 4;
+  const int pos = vt_pos_of_quad(kq);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int w = i >> 1, hi = i & 1;
+    u32x2 x;
+    x[0] = half_of(r.v[0][w], hi) | (half_of(r.v[1][w], hi) << 16);
+    x[1] = half_of(r.v[2][w], hi) | (half_of(r.v[3][w], hi) << 16);
+    *(u32x2*)(Vt + (8 * dc + i) * kVPitch + pos) = x;
+  }
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void sel_attn_mfma(const AttnArgs a) {
+  constexpr int RW = 32 / G;  // selected rows per wavefront
+  constexpr int RT = 4 * RW;  // selected rows per workgroup tile
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kKT * kKPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][128 * kVPitch];
+
+  const int item = blockIdx.x;
+  const int split = item % a.max_splits;
+  const int rest = item / a.max_splits;
+  const int kv = rest % a.Hkv;
+  const int64_t tile = a.n_tiles - 1 - rest / a.Hkv;  // longest rows first
+  const int layer = a.lb + blockIdx.y;
+  const int64_t m0 = tile * RT;
+  const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
+  const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
+  const int key_begin = split * a.split;
+  if (key_begin > g_last) return;  // whole workgroup: this split is past every row
+  const int key_end = min(key_begin + a.split, g_last + 1);
+  const int n_splits_tile = (g_last + a.split) / a.split;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q = lane & 31, hi = lane >> 5;
+  const int64_t m = m0 + wave * RW + q / G;
+  const int h = kv * G + q % G;
+  int g_q = -1;
+  if (m < a.n_sel) {
+    const int t = a.sel[m];
+    if (t >= a.cs1 && t < a.T) g_q = t;
+  }
+  const bool valid = g_q >= 0;
+  // wavefront-wide limits (sel ascending)
+  const int64_t mw0 = m0 + wave * RW;
+  const int64_t mw1 = min(mw0 + RW, a.n_sel) - 1;
+  const int g_wmin = mw0 < a.n_sel ? a.sel[mw0] : 0x7fffffff;
+  const int g_wmax = mw0 < a.n_sel ? a.sel[mw1] : -1;
+
+  bf16x8 qb[8];
+  if (valid) {
+    const uint16_t* qp = a.q + (((int64_t)layer * a.Hq + h) * a.n + (g_q - a.cs1)) * 128 + 8 * hi;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qb[s] = *(const bf16x8*)(qp + 16 * s);
+  } else {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qb[s] = bf16x8{};
+  }
+
+  const uint16_t* kbase = a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128;
+  const uint16_t* vbase = a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128;
+
+  f32x16 o[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) o[d] = f32x16{};
+  float m_use = -INFINITY, l_run = 0.f;
+  const float sc = a.scale_log2;
+
+  const int n_kt = (key_end - key_begin + kKT - 1) / kKT;
+  {
+    TileRegs r;
+    load_tile(r, kbase, vbase, key_begin, a.T, tid);
+    store_tile(r, Ks[0], Vt[0], tid);
+  }
+  __syncthreads();
+
+  for (int it = 0; it < n_kt; ++it) {
+    const int kt = key_begin + it * kKT;
+    const int buf = it & 1;
+    const bool has_next = it + 1 < n_kt;
+    TileRegs nx;
+    if (has_next) load_tile(nx, kbase, vbase, kt + kKT, a.T, tid);
+
+    if (kt <= g_wmax) {  // some row of this wavefront sees keys of the tile
+      const uint16_t* K = Ks[buf];
+      const uint16_t* V = Vt[buf];
+      f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const bf16x8 k0 = *(const bf16x8*)(K + q * kKPitch + 16 * s + 8 * hi);
+        const bf16x8 k1 = *(const bf16x8*)(K + (32 + q) * kKPitch + 16 * s + 8 * hi);
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], s1, 0, 0, 0);
+      }
+      // causal mask: accumulator register r of block b holds key
+      // kt + 32b + 8(r/4) + 4hi + r%4 for this lane's query
+      if (kt + kKT - 1 > g_wmin) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt + 8 * (r >> 2) + 4 * hi + (r & 3);
+          if (key > g_q) s0[r] = -INFINITY;
+          if (key + 32 > g_q) s1[r] = -INFINITY;
+        }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+      const float mt = pair_max(mx) * sc;
+      const bool need = mt > m_use + kRescaleLog2;
+      if (__ballot(need)) {
+        const float m_new = need ? mt : m_use;
+        const float alpha = need ? __builtin_amdgcn_exp2f(m_use - m_new) : 1.f;
+        l_run *= alpha;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) o[d] *= alpha;
+        m_use = m_new;
+      }
+      const float msafe = m_use == -INFINITY ? 0.f : m_use;
+      float lsum = 0.f;
+      f32x16 p0, p1;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        p0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], sc, -msafe));
+        p1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], sc, -msafe));
+        lsum += p0[r] + p1[r];
+      }
+      l_run += lsum;
+      bf16x8 pb[4];
+      {
+        typedef float f32x8 __attribute__((ext_vector_type(8)));
+        f32x8 t;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) t[x] = p0[x];
+        pb[0] = __builtin_convertvector(t, bf16x8);
+#pragma unroll
+        for (int x = 0; x < 8; ++x) t[x] = p0[8 + x];
+        pb[1] = __builtin_convertvector(t, bf16x8);
+#pragma unroll
+        for (int x = 0; x < 8; ++x) t[x] = p1[x];
+        pb[2] = __builtin_convertvector(t, bf16x8);
+#pragma unroll
+        for (int x = 0; x < 8; ++x) t[x] = p1[8 + x];
+        pb[3] = __builtin_convertvector(t, bf16x8);
+      }
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const bf16x8 va = *(const bf16x8*)(V + (32 * d + q) * kVPitch + 16 * ks + 8 * hi);
+          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks], o[d], 0, 0, 0);
+        }
+      }
+    }
+    if (has_next) store_tile(nx, Ks[buf ^ 1], Vt[buf ^ 1], tid);
+    __syncthreads();
+  }
+
+  const float l_tot = pair_sum(l_run);
+  // accumulator register r of d-block b holds dim 32b + 8(r/4) + 4hi + r%4
+  if (n_splits_tile == 1) {
+    if (!valid) return;
+    const float inv = 1.f / l_tot;
+    uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        u32x2 w;
+        w[0] = pack_bf16x2(o[d][4 * rq] * inv, o[d][4 * rq + 1] * inv);
+        w[1] = pack_bf16x2(o[d][4 * rq + 2] * inv, o[d][4 * rq + 3] * inv);
+        *(u32x2*)(op + 32 * d + 8 * rq + 4 * hi) = w;
+      }
+    if (a.lse && hi == 0)
+      a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (m_use + __log2f(l_tot)) * kLn2;
+  } else {
+    const int ql = wave * 32 + q;
+    const int64_t slot = (int64_t)blockIdx.y * gridDim.x + item;
+    float* pp = a.part + (slot * kQPerWG + ql) * 128;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        f32x4 w = {o[d][4 * rq], o[d][4 * rq + 1], o[d][4 * rq + 2], o[d][4 * rq + 3]};
+        *(f32x4*)(pp + 32 * d + 8 * rq + 4 * hi) = w;
+      }
+    if (hi == 0) {
+      float* ml = a.part_ml + (slot * kQPerWG + ql) * 2;
+      ml[0] = m_use;
+      ml[1] = l_tot;
+    }
+  }
+}
+
+// Merge the key splits of every multi-split tile.
+template <int G>
+__global__ __launch_bounds__(256) void sel_attn_combine(const AttnArgs a) {
+  constexpr int RW = 32 / G;
+  constexpr int RT = 4 * RW;
+  const int rest = blockIdx.x;
+  const int kv = rest % a.Hkv;
+  const int64_t tile = a.n_tiles - 1 - rest / a.Hkv;
+  const int layer = a.lb + blockIdx.y;
+  const int64_t m0 = tile * RT;
+  const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
+  const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
+  const int ns = (g_last + a.split) / a.split;
+  if (ns <= 1) return;
+  const int64_t items = (int64_t)gridDim.x * a.max_splits;
+  const int64_t slot0 = (int64_t)blockIdx.y * items + (int64_t)rest * a.max_splits;
+  for (int idx = threadIdx.x; idx < kQPerWG * 32; idx += blockDim.x) {
+    const int ql = idx >> 5, d4 = idx & 31;
+    const int wave = ql >> 5, q = ql & 31;
+    const int64_t m = m0 + wave * RW + q / G;
+    if (m >= a.n_sel) continue;
+    const int h = kv * G + q % G;
+    float M = -INFINITY;
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, a.part_ml[((slot0 + s) * kQPerWG + ql) * 2]);
+    float L = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < ns; ++s) {
+      const float ms = a.part_ml[((slot0 + s) * kQPerWG + ql) * 2];
+      const float ls = a.part_ml[((slot0 + s) * kQPerWG + ql) * 2 + 1];
+      const float w = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M);
+      L += w * ls;
+      const f32x4 po = *(const f32x4*)(a.part + ((slot0 + s) * kQPerWG + ql) * 128 + 4 * d4);
+      acc += w * po;
+    }
+    const float inv = 1.f / L;
+    uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128 + 4 * d4;
+    u32x2 w2;
+    w2[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+    w2[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+    *(u32x2*)op = w2;
+    if (a.lse && d4 == 0) a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (M + __log2f(L)) * kLn2;
+  }
+}
+
+// ============================================================== generic attention
+struct GenAttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* sel;
+  void* out;
+  float* lse;
+  int64_t T, n, n_sel;
+  int cs1, Hq, Hkv, G, D, lb;
+  float scale;
+};
+
+template <typename E>
+__device__ __forceinline__ float gld(const E* p);
+template <>
+__device__ __forceinline__ float gld<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float gld<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+template <typename E>
+__device__ __forceinline__ void gst(E* p, float x);
+template <>
+__device__ __forceinline__ void gst<float>(float* p, float x) { *p = x; }
+template <>
+__device__ __forceinline__ void gst<uint16_t>(uint16_t* p, float x) { *p = f32_to_bf16(x); }
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+template <typename E>
+__global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a) {
+  __shared__ float qs[512];
+  __shared__ float ps[64];
+  const int64_t m = blockIdx.x;
+  const int h = blockIdx.y;
+  const int layer = a.lb + blockIdx.z;
+  const int lane = threadIdx.x;
+  const int t = a.sel[m];
+  if (t < a.cs1 || t >= a.T) return;  // out-of-contract index
+  const int kv = h / a.G;
+  const E* qp = (const E*)a.q + (((int64_t)layer * a.Hq + h) * a.n + (t - a.cs1)) * a.D;
+  const E* kb = (const E*)a.k + ((int64_t)layer * a.Hkv + kv) * a.T * a.D;
+  const E* vb = (const E*)a.v + ((int64_t)layer * a.Hkv + kv) * a.T * a.D;
+  for (int d = lane; d < a.D; d += 64) qs[d] = gld(qp + d);
+  __syncthreads();
+  float acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+  float mrun = -INFINITY, lrun = 0.f;
+  for (int j0 = 0; j0 <= t; j0 += 64) {
+    const int j = j0 + lane;
+    float s = -INFINITY;
+    if (j <= t) {
+      const E* kr = kb + (int64_t)j * a.D;
+      float dot = 0.f;
+      for (int d = 0; d < a.D; ++d) dot = fmaf(qs[d], gld(kr + d), dot);
+      s = dot * a.scale;
+    }
+    const float m_new = fmaxf(mrun, wave_max(s));
+    const float alpha = mrun == -INFINITY ? 0.f : expf(mrun - m_new);
+    const float p = j <= t ? expf(s - m_new) : 0.f;
+    lrun = lrun * alpha + wave_sum(p);
+#pragma unroll
+    for (int x = 0; x < 8; ++x) acc[x] *= alpha;
+    ps[lane] = p;
+    __syncthreads();
+    const int cnt = min(64, t + 1 - j0);
+    for (int jj = 0; jj < cnt; ++jj) {
+      const float pj = ps[jj];
+      const E* vr = vb + (int64_t)(j0 + jj) * a.D;
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        const int d = lane + 64 * x;
+        if (d < a.D) acc[x] = fmaf(pj, gld(vr + d), acc[x]);
+      }
+    }
+    __syncthreads();
+    mrun = m_new;
+  }
+  E* op = (E*)a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * a.D;
+  const float inv = 1.f / lrun;
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    const int d = lane + 64 * x;
+    if (d < a.D) gst(op + d, acc[x] * inv);
+  }
+  if (a.lse && lane == 0) a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = mrun + logf(lrun);
+}
+
+// ============================================================== planning & launch
+static int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+AttnPlan plan_attention(const Geo& g, int64_t n_sel) {
+  AttnPlan p{};
+  p.mfma = g.dtype == CS_BF16 && g.D == 128 && g.G <= 32 && 32 % g.G == 0;
+  if (!p.mfma || n_sel == 0) {
+    p.split = (int)round_up(g.T, kKT);
+    p.max_splits = 1;
+    p.ws_bytes_per_layer = 0;
+    return p;
+  }
+  p.rows_per_tile = 4 * (32 / g.G);
+  p.n_tiles = (n_sel + p.rows_per_tile - 1) / p.rows_per_tile;
+  // Spread the key work over about 2048 workgroups per layer.
+  const int64_t avg_keys = (g.cs1 + g.T) / 2 + 1;
+  const int64_t est = p.n_tiles * g.Hkv * avg_keys;
+  int64_t split = round_up(std::max<int64_t>(1024, (est + 2047) / 2048), kKT);
+  if (split >= g.T) split = round_up(g.T, kKT);
+  p.split = (int)split;
+  p.max_splits = (int)((g.T + split - 1) / split);
+  p.ws_bytes_per_layer =
+      p.max_splits > 1 ? (size_t)p.n_tiles * g.Hkv * p.max_splits * kQPerWG * (128 + 2) * sizeof(float) : 0;
+  return p;
+}
+
+template <int G>
+static void launch_mfma_g(const AttnArgs& a, int64_t items, int layers, hipStream_t s) {
+  {
+    TraceScope tr("sel_attn_mfma", s);
+    hipLaunchKernelGGL(sel_attn_mfma<G>, dim3((unsigned)items, layers), dim3(256), 0, s, a);
+  }
+  if (a.max_splits > 1) {
+    TraceScope tr("sel_attn_combine", s);
+    hipLaunchKernelGGL(sel_attn_combine<G>, dim3((unsigned)(a.n_tiles * a.Hkv), layers), dim3(256), 0, s, a);
+  }
+}
+
+cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const void* v, int lb, int le,
+                           const int32_t* sel, int64_t n_sel, const void* qf, void* out, float* lse, void* ws,
+                           hipStream_t s) {
+  const int layers = le - lb;
+  if (p.mfma) {
+    AttnArgs a;
+    a.q = (const uint16_t*)qf;
+    a.k = (const uint16_t*)k;
+    a.v = (const uint16_t*)v;
+    a.sel = sel;
+    a.out = (uint16_t*)out;
+    a.lse = lse;
+    const int64_t items = p.n_tiles * g.Hkv * p.max_splits;
+    a.part = (float*)ws;
+    a.part_ml = a.part ? a.part + (size_t)layers * items * kQPerWG * 128 : nullptr;
+    a.T = g.T;
+    a.n = g.n;
+    a.n_sel = n_sel;
+    a.n_tiles = p.n_tiles;
+    a.cs1 = (int)g.cs1;
+    a.Hq = g.Hq;
+    a.Hkv = g.Hkv;
+    a.lb = lb;
+    a.split = p.split;
+    a.max_splits = p.max_splits;
+    a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g.D));
+    switch (g.G) {
+      case 1: launch_mfma_g<1>(a, items, layers, s); break;
+      case 2: launch_mfma_g<2>(a, items, layers, s); break;
+      case 4: launch_mfma_g<4>(a, items, layers, s); break;
+      case 8: launch_mfma_g<8>(a, items, layers, s); break;
+      case 16: launch_mfma_g<16>(a, items, layers, s); break;
+      case 32: launch_mfma_g<32>(a, items, layers, s); break;
+      default: return fail(CS_ERR_UNSUPPORTED, "MFMA attention needs H_q/H_kv dividing 32");
+    }
+    return check_launch("selective attention launch");
+  }
+  GenAttnArgs a;
+  a.q = qf;
+  a.k = k;
+  a.v = v;
+  a.sel = sel;
+  a.out = out;
+  a.lse = lse;
+  a.T = g.T;
+  a.n = g.n;
+  a.n_sel = n_sel;
+  a.cs1 = (int)g.cs1;
+  a.Hq = g.Hq;
+  a.Hkv = g.Hkv;
+  a.G = g.G;
+  a.D = g.D;
+  a.lb = lb;
+  a.scale = (float)(1.0 / sqrt((double)g.D));
+  TraceScope tr("sel_attn_generic", s);
+  if (g.dtype == CS_BF16)
+    hipLaunchKernelGGL(sel_attn_generic<uint16_t>, dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a);
+  else
+    hipLaunchKernelGGL(sel_attn_generic<float>, dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a);
+  return check_launch("generic attention launch");
+}
+
+}  // namespace cs

@@ -1,0 +1,88 @@
+// Internal helpers shared by the HIP sources of the composition library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "chronostitch.h"
+
+namespace cs {
+
+// ------------------------------------------------------------------ errors
+void set_error(const std::string& msg);
+cs_status fail(cs_status code, const std::string& msg);
+cs_status check_launch(const char* what);
+
+// ------------------------------------------------------------------ tracing
+// Launch helper: brackets a kernel launch with trace events when tracing is on.
+struct TraceScope {
+  TraceScope(const char* name, hipStream_t s);
+  ~TraceScope();
+  const char* name;
+  hipStream_t stream;
+  int slot;
+};
+
+// ------------------------------------------------------------------ geometry
+struct Geo {
+  int L, Hq, Hkv, G, D, P;
+  int sec[3];
+  int dtype;          // cs_dtype
+  int esize;          // bytes per element
+  int64_t T;
+  int N;
+  const int64_t* cs;  // chunk_start (host)
+  int64_t cs1, n;     // first later-chunk token, candidate count
+};
+
+// Validates the geometry; on success fills `out`.
+cs_status check_geometry(const cs_geometry* g, Geo* out);
+
+int64_t n_select(double rho, int64_t n);
+
+// ------------------------------------------------------------------ device-side types
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+// bf16 <-> f32 on packed 32-bit words (element 0 in the low half).
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+// Round two floats to bf16 (nearest even, native v_cvt_pk_bf16_f32) and pack.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  f32x2 v = {lo, hi};
+  bf16x2 b = __builtin_convertvector(v, bf16x2);
+  return __builtin_bit_cast(uint32_t, b);
+}
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ __forceinline__ uint16_t f32_to_bf16(float x) { return (uint16_t)(pack_bf16x2(x, 0.f) & 0xffffu); }
+
+// ------------------------------------------------------------------ launches (per source file)
+cs_status launch_rebase(const Geo& g, void* k, const int32_t* offsets, const double* theta,
+                        hipStream_t s);
+cs_status launch_score_select(const Geo& g, const void* k_layer, const void* k_fresh, float* scores,
+                              int32_t* sel, int64_t k_sel, hipStream_t s);
+cs_status launch_scatter(const Geo& g, void* k, void* v, int lb, int le, const int32_t* sel,
+                         int64_t n_sel, const void* kf, const void* vf, hipStream_t s);
+
+struct AttnPlan {
+  bool mfma;            // bf16, D = 128, 32 % G == 0
+  int rows_per_tile;    // selected rows per workgroup tile
+  int64_t n_tiles;      // per KV head
+  int split;            // keys per split (multiple of 64)
+  int max_splits;       // splits of the longest tile
+  size_t ws_bytes_per_layer;
+};
+AttnPlan plan_attention(const Geo& g, int64_t n_sel);
+cs_status launch_attention(const Geo& g, const AttnPlan& plan, const void* k, const void* v,
+                           int lb, int le, const int32_t* sel, int64_t n_sel, const void* qf,
+                           void* out, float* lse, void* ws, hipStream_t s);
+
+}  // namespace cs

@@ -1,0 +1,247 @@
+// Three-axis delta rotation of stored post-rotary keys, in place (Eq. 3).
+//
+// Chunk c turns rotary pair i of every key it owns by
+//   phi_{c,i} = Delta_c[sigma(i)] * theta_i.
+// Each workgroup first builds its chunk's cos/sin table: the angle is formed
+// in float64, reduced modulo 2*pi (Cody-Waite, three-part constant), its
+// cos/sin taken in float64 and rounded to float32.  The rows are then
+// streamed: every element is read once and written once, so the kernel is
+// bound by HBM bandwidth; the rotation itself is 4 flops per pair.
+#include <math.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "cs_common.h"
+
+namespace cs {
+
+// 2*pi = C1 + C2 + C3 with C1, C2 holding 26 significant bits each, so
+// k*C1 and k*C2 are exact for |k| < 2^27.
+#define CS_TWO_PI_C1 0x1.921fb50000000p+2
+#define CS_TWO_PI_C2 0x1.110b460000000p-24
+#define CS_TWO_PI_C3 0x1.1a62633145c07p-52
+#define CS_INV_TWO_PI 0x1.45f306dc9c883p-3
+
+__device__ __forceinline__ float2 cos_sin_of(double phi) {
+  double k = rint(phi * CS_INV_TWO_PI);
+  double r = phi;
+  if (fabs(k) < 134217728.0) {  // 2^27
+    r = fma(-k, CS_TWO_PI_C1, r);
+    r = fma(-k, CS_TWO_PI_C2, r);
+    r = fma(-k, CS_TWO_PI_C3, r);
+  }
+  double s, c;
+  sincos(r, &s, &c);
+  return make_float2((float)c, (float)s);
+}
+
+__device__ __forceinline__ int axis_of(int i, int sec0, int sec01) {
+  return i < sec0 ? 0 : (i < sec01 ? 1 : 2);
+}
+
+// ---------------------------------------------------------------- bf16, D = 128
+constexpr int kFastMaxChunks = 96;
+constexpr int kFastTB = 64;  // tokens per workgroup
+constexpr int kFastPG = 8;   // planes (layer x kv head) per workgroup
+
+struct RebaseFastArgs {
+  uint16_t* k;
+  int64_t T;
+  int planes;
+  int sec0, sec01;
+  int tblocks;  // token blocks of the longest chunk in this launch
+  double theta[64];
+  int start[kFastMaxChunks];
+  int len[kFastMaxChunks];
+  int off[kFastMaxChunks][3];
+};
+
+__device__ __forceinline__ void rotate8(u32x4& wa, u32x4& wb, const float* c, const float* s) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    float a0 = bf16_lo(wa[w]), a1 = bf16_hi(wa[w]);
+    float b0 = bf16_lo(wb[w]), b1 = bf16_hi(wb[w]);
+    float c0 = c[2 * w], s0 = s[2 * w], c1 = c[2 * w + 1], s1 = s[2 * w + 1];
+    float na0 = fmaf(a0, c0, -b0 * s0), nb0 = fmaf(a0, s0, b0 * c0);
+    float na1 = fmaf(a1, c1, -b1 * s1), nb1 = fmaf(a1, s1, b1 * c1);
+    wa[w] = pack_bf16x2(na0, na1);
+    wb[w] = pack_bf16x2(nb0, nb1);
+  }
+}
+
+// Lane layout: 8 lanes per 256-byte row; lane j of the row owns pairs
+// 8j..8j+7, i.e. 16 bytes in each half of the row.  256 threads cover 32 rows
+// per step; a workgroup covers kFastPG planes x kFastTB tokens (16 steps),
+// issuing four steps' loads before any store.
+__global__ __launch_bounds__(256) void rebase_bf16_d128(const RebaseFastArgs a) {
+  __shared__ float2 tab[64];
+  const int c = blockIdx.y;
+  const int tb = blockIdx.x % a.tblocks;
+  const int pg = blockIdx.x / a.tblocks;
+  const int len = a.len[c];
+  const int t0 = tb * kFastTB;
+  if (t0 >= len) return;  // whole workgroup
+  if (threadIdx.x < 64) {
+    const int i = threadIdx.x;
+    const double phi = (double)a.off[c][axis_of(i, a.sec0, a.sec01)] * a.theta[i];
+    tab[i] = cos_sin_of(phi);
+  }
+  __syncthreads();
+  const int j = threadIdx.x & 7;
+  const int r0 = threadIdx.x >> 3;  // 0..31
+  float cs_[8], sn_[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float2 t = tab[8 * j + e];
+    cs_[e] = t.x;
+    sn_[e] = t.y;
+  }
+  const int64_t base_tok = a.start[c] + t0;
+#pragma unroll 1
+  for (int it = 0; it < (kFastPG * kFastTB) / 32; it += 4) {
+    u32x4 wa[4], wb[4];
+    uint16_t* row[4];
+    bool ok[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = (it + u) * 32 + r0;
+      const int plane = pg * kFastPG + idx / kFastTB;
+      const int tok = idx % kFastTB;
+      ok[u] = plane < a.planes && t0 + tok < len;
+      row[u] = a.k + ((int64_t)plane * a.T + base_tok + tok) * 128;
+      if (ok[u]) {
+        wa[u] = *(const u32x4*)(row[u] + 8 * j);
+        wb[u] = *(const u32x4*)(row[u] + 64 + 8 * j);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (ok[u]) {
+        rotate8(wa[u], wb[u], cs_, sn_);
+        *(u32x4*)(row[u] + 8 * j) = wa[u];
+        *(u32x4*)(row[u] + 64 + 8 * j) = wb[u];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- generic
+constexpr int kGenMaxChunks = 32;
+constexpr int kGenTB = 32;
+
+struct RebaseGenArgs {
+  void* k;
+  int64_t T;
+  int planes, D, P;
+  int sec0, sec01;
+  int tblocks;
+  double theta[256];
+  int start[kGenMaxChunks];
+  int len[kGenMaxChunks];
+  int off[kGenMaxChunks][3];
+};
+
+template <typename E>
+__device__ __forceinline__ float ld(const E* p);
+template <>
+__device__ __forceinline__ float ld<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float ld<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+template <typename E>
+__device__ __forceinline__ void st(E* p, float x);
+template <>
+__device__ __forceinline__ void st<float>(float* p, float x) { *p = x; }
+template <>
+__device__ __forceinline__ void st<uint16_t>(uint16_t* p, float x) { *p = f32_to_bf16(x); }
+
+template <typename E>
+__global__ __launch_bounds__(256) void rebase_generic(const RebaseGenArgs a) {
+  __shared__ float2 tab[256];
+  const int c = blockIdx.y;
+  const int tb = blockIdx.x % a.tblocks;
+  const int plane = blockIdx.x / a.tblocks;
+  const int len = a.len[c];
+  const int t0 = tb * kGenTB;
+  if (t0 >= len || plane >= a.planes) return;
+  for (int i = threadIdx.x; i < a.P; i += blockDim.x) {
+    const double phi = (double)a.off[c][axis_of(i, a.sec0, a.sec01)] * a.theta[i];
+    tab[i] = cos_sin_of(phi);
+  }
+  __syncthreads();
+  E* k = (E*)a.k;
+  const int ntok = min(kGenTB, len - t0);
+  for (int w = threadIdx.x; w < ntok * a.P; w += blockDim.x) {
+    const int tok = w / a.P, i = w % a.P;
+    E* row = k + ((int64_t)plane * a.T + a.start[c] + t0 + tok) * a.D;
+    const float x = ld(row + i), y = ld(row + i + a.P);
+    const float2 t = tab[i];
+    st(row + i, fmaf(x, t.x, -y * t.y));
+    st(row + i + a.P, fmaf(x, t.y, y * t.x));
+  }
+}
+
+// ---------------------------------------------------------------- host launcher
+cs_status launch_rebase(const Geo& g, void* k, const int32_t* off, const double* theta,
+                        hipStream_t s) {
+  std::vector<int> todo;
+  for (int c = 0; c < g.N; ++c)
+    if (off[3 * c] || off[3 * c + 1] || off[3 * c + 2]) todo.push_back(c);
+  const int planes = g.L * g.Hkv;
+  const bool fast = g.dtype == CS_BF16 && g.D == 128;
+  const int per = fast ? kFastMaxChunks : kGenMaxChunks;
+  for (size_t b = 0; b < todo.size(); b += per) {
+    const int nc = (int)std::min<size_t>(per, todo.size() - b);
+    int maxlen = 0;
+    for (int q = 0; q < nc; ++q) {
+      const int c = todo[b + q];
+      maxlen = std::max<int>(maxlen, (int)(g.cs[c + 1] - g.cs[c]));
+    }
+    if (fast) {
+      RebaseFastArgs a;
+      a.k = (uint16_t*)k;
+      a.T = g.T;
+      a.planes = planes;
+      a.sec0 = g.sec[0];
+      a.sec01 = g.sec[0] + g.sec[1];
+      a.tblocks = (maxlen + kFastTB - 1) / kFastTB;
+      for (int i = 0; i < 64; ++i) a.theta[i] = theta[i];
+      for (int q = 0; q < nc; ++q) {
+        const int c = todo[b + q];
+        a.start[q] = (int)g.cs[c];
+        a.len[q] = (int)(g.cs[c + 1] - g.cs[c]);
+        for (int x = 0; x < 3; ++x) a.off[q][x] = off[3 * c + x];
+      }
+      const int pgroups = (planes + kFastPG - 1) / kFastPG;
+      TraceScope tr("rebase_bf16_d128", s);
+      hipLaunchKernelGGL(rebase_bf16_d128, dim3(a.tblocks * pgroups, nc), dim3(256), 0, s, a);
+    } else {
+      RebaseGenArgs a;
+      a.k = k;
+      a.T = g.T;
+      a.planes = planes;
+      a.D = g.D;
+      a.P = g.P;
+      a.sec0 = g.sec[0];
+      a.sec01 = g.sec[0] + g.sec[1];
+      a.tblocks = (maxlen + kGenTB - 1) / kGenTB;
+      for (int i = 0; i < g.P; ++i) a.theta[i] = theta[i];
+      for (int q = 0; q < nc; ++q) {
+        const int c = todo[b + q];
+        a.start[q] = (int)g.cs[c];
+        a.len[q] = (int)(g.cs[c + 1] - g.cs[c]);
+        for (int x = 0; x < 3; ++x) a.off[q][x] = off[3 * c + x];
+      }
+      TraceScope tr("rebase_generic", s);
+      if (g.dtype == CS_BF16)
+        hipLaunchKernelGGL(rebase_generic<uint16_t>, dim3(a.tblocks * planes, nc), dim3(256), 0, s, a);
+      else
+        hipLaunchKernelGGL(rebase_generic<float>, dim3(a.tblocks * planes, nc), dim3(256), 0, s, a);
+    }
+    cs_status st = check_launch("rebase kernel launch");
+    if (st) return st;
+  }
+  return CS_OK;
+}
+
+}  // namespace cs

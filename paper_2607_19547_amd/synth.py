@@ -55,6 +55,7 @@ class Workload:
     offsets: str               # offset recipe name
     seed: int = 0
     rhos: tuple = field(default=())
+    chunk_lens: tuple = field(default=())   # ragged chunks: explicit token counts (overrides the grid)
 
     @property
     def chunk_tokens(self):
@@ -62,16 +63,18 @@ class Workload:
         return t * h * w
 
     @property
-    def n_tokens(self):
-        return self.chunk_tokens * self.n_chunks
-
-    @property
     def chunk_start(self):
+        if self.chunk_lens:
+            return np.concatenate([[0], np.cumsum(self.chunk_lens)]).astype(np.int64)
         return np.arange(self.n_chunks + 1, dtype=np.int64) * self.chunk_tokens
 
     @property
+    def n_tokens(self):
+        return int(self.chunk_start[-1])
+
+    @property
     def cs1(self):
-        return self.chunk_tokens
+        return int(self.chunk_start[1])
 
     @property
     def n_candidates(self):
@@ -102,18 +105,24 @@ def _rng(seed, stream, tag, layer=0):
 
 
 def local_coords(w: Workload):
-    """Local (t, h, w) of every token: raster order inside each chunk, from 0."""
-    tg, hh, ww = w.chunk_grid
-    j = np.arange(w.chunk_tokens, dtype=np.int64)
-    one = np.stack([j // (hh * ww), (j // ww) % hh, j % ww], axis=-1)
-    return np.tile(one, (w.n_chunks, 1))
+    """Local (t, h, w) of every token: raster order inside each chunk, from 0
+    (a ragged chunk ends with a partial frame)."""
+    _, hh, ww = w.chunk_grid
+    cs = w.chunk_start
+    parts = []
+    for c in range(w.n_chunks):
+        j = np.arange(cs[c + 1] - cs[c], dtype=np.int64)
+        parts.append(np.stack([j // (hh * ww), (j // ww) % hh, j % ww], axis=-1))
+    return np.concatenate(parts)
 
 
 def chunk_offsets(w: Workload):
     """Per-chunk global offsets (dt, dh, dw) = p' - p, int64 [N, 3]."""
     N = w.n_chunks
     off = np.zeros((N, 3), dtype=np.int64)
-    if w.offsets == "tiny":
+    if w.offsets == "none":
+        pass
+    elif w.offsets == "tiny":
         off[1] = (2, 0, 0)
     elif w.offsets == "cumulative8":
         off[:, 0] = 8 * np.arange(N)
@@ -132,25 +141,29 @@ def chunk_offsets(w: Workload):
 
 
 def draw_normal(shape, seed, stream, tag, layer=0, std=1.0):
-    """float64 N(0, std^2) draw of one tensor slice (one layer)."""
-    return _rng(seed, stream, tag, layer).standard_normal(shape) * std
+    """N(0, std^2) draw of one tensor slice (one layer): float32 samples
+    returned as float64."""
+    x = _rng(seed, stream, tag, layer).standard_normal(shape, dtype=np.float32).astype(np.float64)
+    return x * std if std != 1.0 else x
 
 
-def draw_layer(w: Workload, layer):
-    """All random tensors of one layer, float64, pre-rotary.
+LAYER_TENSORS = ("k_pre", "v", "zk", "zv", "q_pre")
+
+
+def draw_layer(w: Workload, layer, which=LAYER_TENSORS):
+    """Random tensors of one layer, float64, pre-rotary.
 
     k_pre, v     [H_kv, T, D]   stored keys (before rotation) and values
     zk, zv       [H_kv, n, D]   fresh-row noise, N(0, 0.1^2)
     q_pre        [H_q, n, D]    fresh queries (before rotation)
     """
     T, n, D = w.n_tokens, w.n_candidates, w.head_dim
-    return dict(
-        k_pre=draw_normal((w.n_kv_heads, T, D), w.seed, 0, TAG_K, layer),
-        v=draw_normal((w.n_kv_heads, T, D), w.seed, 0, TAG_V, layer),
-        zk=draw_normal((w.n_kv_heads, n, D), w.seed, 1, TAG_ZK, layer, 0.1),
-        zv=draw_normal((w.n_kv_heads, n, D), w.seed, 1, TAG_ZV, layer, 0.1),
-        q_pre=draw_normal((w.n_q_heads, n, D), w.seed, 2, TAG_Q, layer),
-    )
+    spec = dict(k_pre=((w.n_kv_heads, T, D), 0, TAG_K, 1.0),
+                v=((w.n_kv_heads, T, D), 0, TAG_V, 1.0),
+                zk=((w.n_kv_heads, n, D), 1, TAG_ZK, 0.1),
+                zv=((w.n_kv_heads, n, D), 1, TAG_ZV, 0.1),
+                q_pre=((w.n_q_heads, n, D), 2, TAG_Q, 1.0))
+    return {k: draw_normal(spec[k][0], w.seed, spec[k][1], spec[k][2], layer, spec[k][3]) for k in which}
 
 
 def draw_token_scale(w: Workload):

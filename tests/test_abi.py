@@ -1,0 +1,133 @@
+"""The C-ABI library loads on a host without a GPU, exports every function the
+header declares, and rejects invalid arguments with the documented status
+before touching the device (no GPU needed: validation runs before any HIP call)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2607_19547_amd import binding as b
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "chronostitch.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(\w+)\s*\(", src, flags=re.M)))
+
+
+def test_header_declares_the_three_entry_points():
+    names = declared_functions()
+    for n in ("compose_rebase_k", "score_deviation_topk", "selective_attend_scatter", "cs_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(built_lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", built_lib], capture_output=True, text=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    L = b.lib()
+    for n in declared_functions():
+        assert hasattr(L, n)
+
+
+def _geo(**kw):
+    d = dict(n_layers=2, n_q_heads=4, n_kv_heads=2, head_dim=16, sections=(2, 3, 3), dtype="f32",
+             chunk_start=[0, 32, 64])
+    d.update(kw)
+    return b.Geo(**d)
+
+
+def _code(fn, *a, **kw):
+    with pytest.raises(b.CsError) as e:
+        fn(*a, **kw)
+    return e.value.code, str(e.value)
+
+
+FAKE = type("FakeTensor", (), {"data_ptr": lambda self: 0x1000, "numel": lambda self: 1 << 20,
+                              "element_size": lambda self: 1})()
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(n_kv_heads=3), "multiple"),
+    (dict(head_dim=15, sections=(2, 3, 2)), "even"),
+    (dict(sections=(2, 3, 4)), "sum"),
+    (dict(chunk_start=[0, 40, 30]), "increasing"),
+    (dict(chunk_start=[1, 32, 64]), "chunk_start[0]"),
+    (dict(dtype=7), "dtype"),
+    (dict(n_layers=0), "n_layers"),
+])
+def test_bad_geometry_rejected(built_lib, kw, msg):
+    code, text = _code(b.compose_rebase_k, _geo(**kw), FAKE, np.zeros((2, 3)), stream=0)
+    assert code == b.CS_ERR_INVALID_ARGUMENT and msg in text
+
+
+def test_rebase_argument_errors(built_lib):
+    g = _geo()
+    assert _code(b.compose_rebase_k, g, None, np.zeros((2, 3)), stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    bad_base = b.Geo(2, 4, 2, 16, (2, 3, 3), "f32", [0, 32, 64], rope_base=float("nan"))
+    assert _code(b.compose_rebase_k, bad_base, FAKE, np.zeros((2, 3)), stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+
+
+def test_host_coordinate_shift_without_device_work(built_lib):
+    """global = local + offset of the token's chunk; a geometry with every
+    offset zero enqueues no kernel, so this runs on a CPU-only host."""
+    g = _geo()
+    loc = np.arange(64 * 3, dtype=np.int32).reshape(64, 3)
+    glob = b.compose_rebase_k(g, FAKE, np.zeros((2, 3)), loc, want_global=True, stream=0)
+    assert np.array_equal(glob, loc)
+
+
+@pytest.mark.parametrize("rho", [-0.1, 1.01, float("nan")])
+def test_score_rejects_bad_rho(built_lib, rho):
+    code, _ = _code(b.score_deviation_topk, _geo(), FAKE, 0, FAKE, rho, FAKE, FAKE, stream=0)
+    assert code == b.CS_ERR_INVALID_ARGUMENT
+
+
+def test_score_rejects_bad_layer_and_small_workspace(built_lib):
+    g = _geo()
+    assert _code(b.score_deviation_topk, g, FAKE, 2, FAKE, 0.5, FAKE, FAKE, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    small = type("W", (), {"data_ptr": lambda self: 0x1000, "numel": lambda self: 8,
+                           "element_size": lambda self: 1})()
+    code, _ = _code(b.score_deviation_topk, g, FAKE, 0, FAKE, 0.5, None, FAKE, workspace=small, stream=0)
+    assert code == b.CS_ERR_WORKSPACE_TOO_SMALL
+    assert b.score_deviation_topk_workspace(g) >= 32 * 4
+
+
+def test_score_rho_zero_selects_nothing_on_host(built_lib):
+    """k is computed on the host; a single-chunk cache has no candidates and enqueues nothing."""
+    g = _geo(chunk_start=[0, 64])
+    assert b.score_deviation_topk(g, FAKE, 0, FAKE, 0.5, None, None, stream=0) == 0
+
+
+def test_attention_argument_errors(built_lib):
+    g = _geo()
+    assert _code(b.selective_attend_scatter, g, FAKE, FAKE, 1, 3, FAKE, 4, FAKE, FAKE, FAKE, FAKE,
+                 stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    assert _code(b.selective_attend_scatter, g, FAKE, FAKE, 0, 1, FAKE, 33, FAKE, FAKE, FAKE, FAKE,
+                 stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    assert _code(b.selective_attend_scatter, g, None, FAKE, 0, 1, FAKE, 4, FAKE, FAKE, FAKE, FAKE,
+                 stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    # nothing to do: returns OK without touching the device
+    b.selective_attend_scatter(g, None, None, 0, 1, None, 0, None, None, None, None, stream=0)
+
+
+def test_attention_workspace_sizing(built_lib):
+    q = b.Geo(36, 16, 2, 128, (16, 24, 24), "bf16", np.arange(33) * 2048)
+    one = b.selective_attend_scatter_workspace(q, 6349, 1)
+    assert b.selective_attend_scatter_workspace(q, 6349, 4) == 4 * one
+    assert b.selective_attend_scatter_workspace(q, 0, 1) == 0
+    g = q
+    small = type("W", (), {"data_ptr": lambda self: 0x1000, "numel": lambda self: 16,
+                           "element_size": lambda self: 1})()
+    if one:
+        code, _ = _code(b.selective_attend_scatter, g, FAKE, FAKE, 0, 1, FAKE, 6349, FAKE, FAKE, FAKE,
+                        FAKE, workspace=small, stream=0)
+        assert code == b.CS_ERR_WORKSPACE_TOO_SMALL
+    # the fp32 path needs no workspace
+    assert b.selective_attend_scatter_workspace(_geo(), 8, 1) == 0
