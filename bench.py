@@ -1,0 +1,304 @@
+"""Benchmark of the KV-composition hot path on one MI355X.
+
+One step = one full composition of a 65,536-token, 36-layer Qwen2.5-VL-3B
+shaped bf16 cache (32 chunks x 2048 tokens, 16 query / 2 KV heads, head dim
+128, mRoPE sections 16/24/24) at rho = 0.1:
+  compose_rebase_k -> score_deviation_topk -> 36 x selective_attend_scatter
+(one call per layer, the model's layer-by-layer order).  The caches are
+restored from a pristine copy before every step, outside the timed region
+(re-basing and scattering are in place); each step is bracketed by a device
+synchronisation and HIP events on the stream the library launches on.
+
+Inputs are synthetic and seeded (torch's device generator): stored keys and
+values ~ N(0,1) (a rotation of an isotropic Gaussian is again N(0,1), so the
+stored post-rotary keys are drawn directly), fresh queries ~ N(0,1), fresh
+keys = re-based stored keys + s_t z and fresh values = stored values + s_t z'
+with z, z' ~ N(0, 0.1^2) and s_t ~ LogNormal(0,1) per token.  The re-based
+keys used to build the fresh keys come from one untimed call of the library's
+own compose_rebase_k during set-up.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="long65k")
+    p.add_argument("--rho", type=float, default=None)
+    p.add_argument("--rho1-steps", type=int, default=2, help="steps timed at rho = 1.0 (0: skip)")
+    p.add_argument("--cpu-baseline", type=int, default=1, help="time the CPU oracle on a sample (0: skip)")
+    p.add_argument("--batched-layers", type=int, default=0,
+                   help="one selective_attend_scatter call over all layers instead of one per layer")
+    return p.parse_args()
+
+
+class Inputs:
+    def __init__(self, w, torch, binding, synth):
+        dev = "cuda"
+        bf = torch.bfloat16
+        L, Hkv, Hq, T, D, n = w.n_layers, w.n_kv_heads, w.n_q_heads, w.n_tokens, w.head_dim, w.n_candidates
+        cs1 = w.cs1
+        self.geo = binding.Geo.from_workload(w)
+        self.offsets = synth.chunk_offsets(w)
+        log(f"[bench] generating inputs: L={L} T={T} n={n}")
+        self.K0 = torch.empty((L, Hkv, T, D), dtype=bf, device=dev)
+        self.V0 = torch.empty((L, Hkv, T, D), dtype=bf, device=dev)
+        self.QF = torch.empty((L, Hq, n, D), dtype=bf, device=dev)
+        self.KF = torch.empty((L, Hkv, n, D), dtype=bf, device=dev)
+        self.VF = torch.empty((L, Hkv, n, D), dtype=bf, device=dev)
+        s = synth.torch_token_scale(w, dev)[None, :, None]
+        for layer in range(L):
+            self.K0[layer] = synth.torch_normal((Hkv, T, D), w.seed, 0, synth.TAG_K, layer, dev, bf)
+            self.V0[layer] = synth.torch_normal((Hkv, T, D), w.seed, 0, synth.TAG_V, layer, dev, bf)
+            self.QF[layer] = synth.torch_normal((Hq, n, D), w.seed, 2, synth.TAG_Q, layer, dev, bf)
+        kreb = self.K0.clone()
+        binding.compose_rebase_k(self.geo, kreb, self.offsets)
+        for layer in range(L):
+            zk = synth.torch_normal((Hkv, n, D), w.seed, 1, synth.TAG_ZK, layer, dev, torch.float32, 0.1)
+            zv = synth.torch_normal((Hkv, n, D), w.seed, 1, synth.TAG_ZV, layer, dev, torch.float32, 0.1)
+            self.KF[layer] = (kreb[layer, :, cs1:].float() + s * zk).to(bf)
+            self.VF[layer] = (self.V0[layer, :, cs1:].float() + s * zv).to(bf)
+        del kreb
+        self.K = self.K0.clone()
+        self.V = self.V0.clone()
+        torch.cuda.synchronize()
+
+
+def run_compose(inp, w, rho, binding, torch, out, lse, sel, scores, ws, batched):
+    b = binding
+    b.compose_rebase_k(inp.geo, inp.K, inp.offsets)
+    k = b.score_deviation_topk(inp.geo, inp.K, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
+    if batched:
+        b.selective_attend_scatter(inp.geo, inp.K, inp.V, 0, w.n_layers, sel, k, inp.QF, inp.KF, inp.VF,
+                                   out, lse, ws)
+    else:
+        for layer in range(w.n_layers):
+            b.selective_attend_scatter(inp.geo, inp.K, inp.V, layer, layer + 1, sel, k, inp.QF, inp.KF,
+                                       inp.VF, out, lse, ws)
+    return k
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+              f"multi-GPU path: run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2607_19547_amd import binding, synth
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    binding.lib()
+    w = synth.WORKLOADS[args.workload]
+    rho = w.rho if args.rho is None else args.rho
+    inp = Inputs(w, torch, binding, synth)
+    result = bench_rho(inp, w, rho, args.steps, args.warmup, binding, torch, bool(args.batched_layers))
+    rho1 = None
+    if args.rho1_steps > 0 and rho != 1.0:
+        rho1 = bench_rho(inp, w, 1.0, args.rho1_steps, 1, binding, torch, bool(args.batched_layers))
+    cpu = cpu_baseline(w, rho) if args.cpu_baseline else None
+    emit(args, w, rho, result, rho1, cpu)
+
+
+def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched):
+    b = binding
+    n = w.n_candidates
+    scores = torch.empty(n, dtype=torch.float32, device="cuda")
+    sel = torch.empty(n, dtype=torch.int32, device="cuda")
+    # n_sel is a host-side function of rho and n; one call sizes the buffers
+    k = b.score_deviation_topk(inp.geo, inp.K, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
+    out = torch.empty((w.n_layers, w.n_q_heads, k, w.head_dim), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((w.n_layers, w.n_q_heads, k), dtype=torch.float32, device="cuda")
+    ws_bytes = b.selective_attend_scatter_workspace(inp.geo, k, w.n_layers if batched else 1)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    log(f"[bench] rho={rho}: n_sel={k}, workspace {ws_bytes / 2**20:.1f} MiB, warmup {warmup}, steps {steps}")
+
+    def restore():
+        inp.K.copy_(inp.K0)
+        inp.V.copy_(inp.V0)
+
+    for _ in range(warmup):
+        restore()
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched)
+    torch.cuda.synchronize()
+    b.cs_trace_reset()
+    times = []
+    wall0 = time.perf_counter()
+    for _ in range(steps):
+        restore()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        b.cs_trace_enable(True)
+        e0.record(stream)
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched)
+        e1.record(stream)
+        b.cs_trace_enable(False)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    wall = time.perf_counter() - wall0
+    trace = b.cs_trace_collect()
+    # algorithmic work of the step (from the selection of the last step; outside the timed region)
+    g = sel[:k].cpu().numpy().astype(np.int64)
+    visible = int(np.sum(g + 1))
+    attn_flops_per_layer = 4 * w.head_dim * w.n_q_heads * visible     # QK^T + PV, 2 flops per MAC
+    off = inp.offsets
+    cs = w.chunk_start
+    rot_tokens = int(sum(cs[c + 1] - cs[c] for c in range(w.n_chunks) if np.any(off[c])))
+    rebase_bytes = 2 * w.n_layers * w.n_kv_heads * rot_tokens * w.head_dim * 2   # read + write, bf16
+    res = dict(rho=rho, n_sel=k, ms=float(np.median(times)), ms_mean=float(np.mean(times)),
+               ms_min=float(np.min(times)), wall_s=wall, steps=steps, trace=trace,
+               attn_flops_per_layer=attn_flops_per_layer, rebase_bytes=rebase_bytes, visible=visible)
+    log(f"[bench] rho={rho}: compose median {res['ms']:.3f} ms (min {res['ms_min']:.3f}); kernels:")
+    for name, (cnt, tot) in sorted(trace.items(), key=lambda kv: -kv[1][1]):
+        log(f"    {name:24s} launches {cnt:5d}  avg {tot / cnt * 1e3:9.1f} us  total/step {tot / steps:8.3f} ms")
+    return res
+
+
+def cpu_baseline(w, rho):
+    """The CPU oracle, as it stands, on a bounded sample of the same workload:
+    re-basing and attention of ONE of the 36 layers (the scoring layer) plus the
+    full score and selection, extrapolated to the 36-layer composition."""
+    import oracle
+    from paper_2607_19547_amd import synth
+    log("[bench] cpu_baseline: building one layer of oracle inputs")
+    layer = w.score_layer
+    d = oracle.inputs.build(w, layers=[layer])
+    th = oracle.rope.inv_freq(w.head_dim, w.base)
+    sg = oracle.rope.axis_of_pair(w.sections)
+    t0 = time.perf_counter()
+    k_reb = oracle.rebase.rebase_stored(d["k_stored"], w.dtype, d["chunk_start"], d["chunk_offsets"], th, sg)
+    t_rebase = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    scores = oracle.score.deviation_f32(oracle.bf16.decode(k_reb[0]), oracle.bf16.decode(d["k_fresh"][0]), w.cs1)
+    sel = oracle.select.select_top(scores, oracle.select.n_select(rho, w.n_candidates), w.cs1)
+    t_select = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    kp = oracle.attention.scatter_rows(k_reb[0], d["k_fresh"][0], sel, w.cs1)
+    vp = oracle.attention.scatter_rows(d["v_stored"][0], d["v_fresh"][0], sel, w.cs1)
+    oracle.attention.attend_rows(oracle.bf16.decode(d["q_fresh"][0]), oracle.bf16.decode(kp),
+                                 oracle.bf16.decode(vp), sel, w.cs1)
+    t_attn = time.perf_counter() - t0
+    total_s = w.n_layers * (t_rebase + t_attn) + t_select
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        threads = os.cpu_count()
+    log(f"[bench] cpu_baseline: rebase/layer {t_rebase:.2f} s, score+select {t_select:.2f} s, "
+        f"attention/layer {t_attn:.2f} s -> {total_s:.1f} s per composition (extrapolated)")
+    return dict(value=total_s * 1e3, unit="ms", cores=threads, kind="oracle",
+                sample=(f"1 of {w.n_layers} layers (rebase {t_rebase:.2f} s + scatter/attention "
+                        f"{t_attn:.2f} s, measured) x {w.n_layers} + score/select {t_select:.2f} s "
+                        f"(measured, full); float64 numpy on the host"))
+
+
+def _traffic(kernel):
+    """HBM bytes per launch from the committed rocprofv3 PMC summary, if it was
+    taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(kernel)
+        src = os.path.join(ROOT, "paper_2607_19547_amd", "csrc", rec["source"])
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+            return None
+        return rec["bytes_per_launch"]
+    except Exception:
+        return None
+
+
+def emit(args, w, rho, r, rho1, cpu):
+    tr = r["trace"]
+    steps = r["steps"]
+    attn_n, attn_ms = tr.get("sel_attn_mfma", (0, 0.0))
+    attn_avg_s = attn_ms / max(attn_n, 1) / 1e3
+    attn_tflops = r["attn_flops_per_layer"] / attn_avg_s / 1e12 if attn_n else None
+    reb_n, reb_ms = tr.get("rebase_bf16_d128", (0, 0.0))
+    reb_avg_s = reb_ms / max(reb_n, 1) / 1e3
+    reb_gbps = r["rebase_bytes"] / reb_avg_s / 1e9 if reb_n else None
+    # whole attention stage per layer call: scatter + attention + combine
+    stage = sum(tr.get(k, (0, 0.0))[1] for k in ("scatter_rows", "sel_attn_mfma", "sel_attn_combine"))
+    stage_tflops = w.n_layers * r["attn_flops_per_layer"] / (stage / steps / 1e3) / 1e12 if stage else None
+    line = {
+        "metric": "compose ms/65k-token cache; rebase GB/s (% HBM peak); sel-attn TFLOP/s (% MFMA)",
+        "value": round(r["ms"], 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["ms"], 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": (f"{w.name}: Qwen2.5-VL-3B-shaped bf16 cache, {w.n_layers} layers, "
+                                f"{w.n_q_heads}Q/{w.n_kv_heads}KV heads, head_dim {w.head_dim}, "
+                                f"{w.n_chunks} chunks x {w.chunk_tokens} = {w.n_tokens} tokens, rho={rho}"),
+                   "n_sel": r["n_sel"], "layer_calls": "batched" if args.batched_layers else "per-layer"},
+        "rebase_GBps": None if reb_gbps is None else round(reb_gbps, 1),
+        "rebase_frac_hbm": None if reb_gbps is None else round(reb_gbps / HBM_PEAK_GBPS, 4),
+        "sel_attn_TFLOPs": None if attn_tflops is None else round(attn_tflops, 1),
+        "sel_attn_frac_mfma": None if attn_tflops is None else round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+        "sel_attn_stage_TFLOPs": None if stage_tflops is None else round(stage_tflops, 1),
+        "kernels_ms_per_step": {k: round(v[1] / steps, 4) for k, v in tr.items()},
+        "roofline": {
+            "kernel": "sel_attn_mfma",
+            "bound": "mfma",
+            "achieved": None if attn_tflops is None else round(attn_tflops, 2),
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": None if attn_tflops is None else round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": _traffic("sel_attn_mfma"),
+            "flops_per_launch": r["attn_flops_per_layer"],
+            "avg_launch_us": round(attn_avg_s * 1e6, 2),
+        },
+        "roofline_rebase": {
+            "kernel": "rebase_bf16_d128",
+            "bound": "hbm",
+            "achieved": None if reb_gbps is None else round(reb_gbps, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": None if reb_gbps is None else round(reb_gbps / HBM_PEAK_GBPS, 4),
+            "traffic": _traffic("rebase_bf16_d128"),
+            "bytes_per_launch": r["rebase_bytes"],
+            "avg_launch_us": round(reb_avg_s * 1e6, 2),
+        },
+    }
+    if rho1 is not None:
+        line["rho1_compose_ms"] = round(rho1["ms"], 3)
+        line["rho1_over_rho_speedup"] = round(rho1["ms"] / r["ms"], 3)
+    if cpu is not None:
+        line["cpu_baseline"] = cpu
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

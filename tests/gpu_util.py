@@ -39,5 +39,13 @@ def pair_norm(x):
     return np.concatenate([pn, pn], axis=-1)
 
 
+def ulp(x, dtype):
+    """Spacing of the storage format at |x| (bf16: 8 significant bits, float32: 24)."""
+    mant, emin = (7, -126) if dtype == "bf16" else (23, -126)
+    _, e = np.frexp(np.abs(np.asarray(x, dtype=np.float64)))
+    lead = np.maximum(e.astype(np.int64) - 1, emin)
+    return np.ldexp(1.0, lead - mant)
+
+
 def log(*a):
     print(*a, flush=True)

@@ -2,9 +2,13 @@
 oracle on the same seeded inputs.
 
 Bars (floating point, from the arithmetic of each stage):
-  rebased K      per element |gpu - oracle| <= 2^-8 |pair| (bf16: one rounding
-                 of a float32 rotation vs one of the exact one) or 2^-20 |pair|
-                 (float32 storage); chunks with Delta = 0 bit-exact
+  rebased K      per element |gpu - oracle| <= 1 ulp of the storage format at
+                 the oracle's value + 2^-20 |pair|: both sides round once to
+                 the storage format (which can land on adjacent values), and
+                 the GPU's float32 rotation with float32 cos/sin tables adds an
+                 absolute error of a few 2^-24 |pair|.  Also max abs
+                 <= 2^-8 |k| with |k| the norm of the whole key row.  Chunks
+                 with Delta = 0 are bit-exact
   scores         float32, bit-exact when both sides read the same keys
   selection      index work: bit-exact on the same scores
   scatter        K/V rows bit-exact
@@ -22,7 +26,7 @@ import pytest
 import oracle
 from oracle import bf16 as obf
 from paper_2607_19547_amd import synth
-from tests.gpu_util import empty, log, pair_norm, rel_l2, to_dev, to_host
+from tests.gpu_util import empty, log, pair_norm, rel_l2, to_dev, to_host, ulp
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -52,9 +56,13 @@ def theta_sigma(w):
 def assert_rebase_close(w, got, want, stored):
     """got/want/stored: storage arrays [L, H, T, D]."""
     g, o = dec(got, w.dtype), dec(want, w.dtype)
-    tol = (2.0 ** -8 if w.dtype == "bf16" else 2.0 ** -20) * pair_norm(o) + 2.0 ** -126
-    bad = np.abs(g - o) > tol
-    assert not bad.any(), f"{bad.sum()} elements outside the rebase bound"
+    err = np.abs(g - o)
+    tol = ulp(o, w.dtype) + 2.0 ** -20 * pair_norm(o)
+    bad = err > tol
+    assert not bad.any(), (f"{bad.sum()} elements outside the rebase bound; worst err/ulp "
+                           f"{np.max(err / ulp(o, w.dtype)):.3f}")
+    row = np.sqrt(np.sum(o * o, axis=-1, keepdims=True))
+    assert np.all(err <= 2.0 ** -8 * row + 2.0 ** -126)
     off = synth.chunk_offsets(w)
     cs = w.chunk_start
     for c in range(w.n_chunks):
@@ -141,7 +149,13 @@ def test_tiny_chained_and_isolated():
     assert g["k"] == len(ref["sel"]) == 8
     assert np.allclose(g["scores"], ref["scores"], rtol=1e-5)
     assert g["sel"].tolist() == ref["sel"].tolist()
-    assert np.array_equal(g["k_post"], ref["k_post"]) or g["sel"].tolist() != ref["sel"].tolist()
+    # scatter: selected rows are the fresh rows, every other row is the GPU's rebased row
+    sel = g["sel"]
+    rest = np.setdiff1d(np.arange(w.n_tokens), sel)
+    assert np.array_equal(g["k_post"][:, :, sel], d["k_fresh"][:, :, sel - w.cs1])
+    assert np.array_equal(g["v_post"][:, :, sel], d["v_fresh"][:, :, sel - w.cs1])
+    assert np.array_equal(g["k_post"][:, :, rest], g["k_rebased"][:, :, rest])
+    assert np.array_equal(g["v_post"][:, :, rest], d["v_stored"][:, :, rest])
     o_ref, lse_ref = ref["attn"][0]
     check_attention(w, g["out"][0], g["lse"][0], o_ref, lse_ref, "tiny chained")
     # stage-isolated attention on the oracle's caches and selection
