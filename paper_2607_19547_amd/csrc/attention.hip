@@ -25,6 +25,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "cs_common.h"
 
@@ -96,12 +97,13 @@ cs_status launch_scatter(const Geo& g, void* k, void* v, int lb, int le, const i
 }
 
 // ============================================================== MFMA attention
-constexpr int kKT = 64;       // keys per tile
-constexpr int kKPitch = 136;  // LDS row pitch of K, bf16 elements (128 + 8)
-constexpr int kVPitch = 72;   // LDS row pitch of V^T, bf16 elements (64 + 8)
-constexpr int kQPerWG = 128;  // query vectors per workgroup
+constexpr int kKT = 64;                  // keys per tile
+constexpr int kWaves = 8;                // wavefronts per workgroup (2 per SIMD)
+constexpr int kThreads = 64 * kWaves;
+constexpr int kQPerWG = 32 * kWaves;     // query vectors per workgroup
+constexpr int kRow = 256;                // bytes of one K/V row (bf16 x 128)
 constexpr float kLn2 = 0.69314718055994530942f;
-constexpr float kRescaleLog2 = 8.0f;  // lazy rescale threshold (max growth 2^8)
+constexpr float kRescaleLog2 = 8.0f;     // lazy rescale threshold (max growth 2^8)
 
 struct AttnArgs {
   const uint16_t* q;
@@ -110,13 +112,15 @@ struct AttnArgs {
   const int32_t* sel;
   uint16_t* out;
   float* lse;
-  float* part;     // [layers in call][items][128][128] partial O (unnormalised)
-  float* part_ml;  // [layers in call][items][128][2] running max (log2 units), sum
+  float* part;     // [layers in call][items][kQPerWG][128] partial O (unnormalised)
+  float* part_ml;  // [layers in call][items][kQPerWG][2] running max (log2 units), sum
   int64_t T, n, n_sel, n_tiles;
   int cs1, Hq, Hkv, lb;
   int split, max_splits;
   float scale_log2;  // log2(e) / sqrt(D)
 };
+
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 // Lanes l and l^32 hold the same query: combine their values.
 __device__ __forceinline__ float pair_max(float x) {
@@ -128,57 +132,46 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Position of key j (0..63) inside a V^T row: within each 16-key group the
-// keys a lane half contributes to one MFMA k-step sit next to each other.
-__device__ __forceinline__ int vt_pos_of_quad(int kq) {
-  return 16 * (kq >> 2) + 8 * (kq & 1) + 4 * ((kq >> 1) & 1);
-}
-
-__device__ __forceinline__ uint32_t half_of(uint32_t w, int hi) { return hi ? (w >> 16) : (w & 0xffffu); }
-
-struct TileRegs {
-  u32x4 k[4];
-  u32x4 v[4];
+// LDS tiles are row-major (one 256-byte row per key) with the 16-byte chunks
+// of each row permuted so that the operand reads are free of bank conflicts:
+//   K: chunk c of row r sits at position c ^ (r & 15)   (16 rows, same chunk)
+//   V: chunk c of row r sits at position c ^ 4(r & 3)   (4 rows x 4 chunks)
+// A 64-key tile is 2 x 16 KB; each of the 512 threads stages two 16-byte
+// chunks of K and two of V through registers (sixteen consecutive threads
+// read one 256-byte row, so global reads are fully coalesced).
+struct Stage {
+  u32x4 k[2], v[2];
 };
 
-__device__ __forceinline__ void load_tile(TileRegs& r, const uint16_t* kb, const uint16_t* vb, int kt,
-                                          int64_t T, int tid) {
-  const int c = tid & 15, rr = tid >> 4;
+__device__ __forceinline__ void stage_load(Stage& st, const uint16_t* kb, const uint16_t* vb, int kt,
+                                           int64_t T, int tid) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int key = kt + rr + 16 * j;
-    r.k[j] = key < T ? *(const u32x4*)(kb + (int64_t)key * 128 + 8 * c) : u32x4{0, 0, 0, 0};
-  }
-  const int kq = tid & 15, dc = tid >> 4;
-#pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const int key = kt + 4 * kq + a;
-    r.v[a] = key < T ? *(const u32x4*)(vb + (int64_t)key * 128 + 8 * dc) : u32x4{0, 0, 0, 0};
+  for (int j = 0; j < 2; ++j) {
+    const int ci = tid + kThreads * j;
+    int key = kt + (ci >> 4);
+    key = key < T ? key : (int)T - 1;  // rows past the cache are masked; keep the address inside it
+    st.k[j] = *(const u32x4*)(kb + (int64_t)key * 128 + 8 * (ci & 15));
+    st.v[j] = *(const u32x4*)(vb + (int64_t)key * 128 + 8 * (ci & 15));
   }
 }
 
-__device__ __forceinline__ void store_tile(const TileRegs& r, uint16_t* Ks, uint16_t* Vt, int tid) {
-  const int c = tid & 15, rr = tid >> 4;
+__device__ __forceinline__ void stage_store(const Stage& st, char* Ks, char* Vs, int tid) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) *(u32x4*)(Ks + (rr + 16 * j) * kKPitch + 8 * c) = r.k[j];
-  const int kq = tid & 15, dc = tid >> 4;
-  const int pos = vt_pos_of_quad(kq);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int w = i >> 1, hi = i & 1;
-    u32x2 x;
-    x[0] = half_of(r.v[0][w], hi) | (half_of(r.v[1][w], hi) << 16);
-    x[1] = half_of(r.v[2][w], hi) | (half_of(r.v[3][w], hi) << 16);
-    *(u32x2*)(Vt + (8 * dc + i) * kVPitch + pos) = x;
+  for (int j = 0; j < 2; ++j) {
+    const int ci = tid + kThreads * j;
+    const int row = ci >> 4, c = ci & 15;
+    *(u32x4*)(Ks + row * kRow + 16 * (c ^ (row & 15))) = st.k[j];
+    *(u32x4*)(Vs + row * kRow + 16 * (c ^ ((row & 3) << 2))) = st.v[j];
   }
 }
 
 template <int G>
-__global__ __launch_bounds__(256) void sel_attn_mfma(const AttnArgs a) {
-  constexpr int RW = 32 / G;  // selected rows per wavefront
-  constexpr int RT = 4 * RW;  // selected rows per workgroup tile
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kKT * kKPitch];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][128 * kVPitch];
+__global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
+  constexpr int RW = 32 / G;       // selected rows per wavefront
+  constexpr int RT = kWaves * RW;  // selected rows per workgroup tile
+  constexpr int kBufs = 3;
+  __shared__ __attribute__((aligned(1024))) char Ks[kBufs][kKT * kRow];
+  __shared__ __attribute__((aligned(1024))) char Vs[kBufs][kKT * kRow];
 
   const int item = blockIdx.x;
   const int split = item % a.max_splits;
@@ -204,11 +197,23 @@ __global__ __launch_bounds__(256) void sel_attn_mfma(const AttnArgs a) {
     if (t >= a.cs1 && t < a.T) g_q = t;
   }
   const bool valid = g_q >= 0;
-  // wavefront-wide limits (sel ascending)
   const int64_t mw0 = m0 + wave * RW;
   const int64_t mw1 = min(mw0 + RW, a.n_sel) - 1;
   const int g_wmin = mw0 < a.n_sel ? a.sel[mw0] : 0x7fffffff;
   const int g_wmax = mw0 < a.n_sel ? a.sel[mw1] : -1;
+
+  const uint16_t* kbase = a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128;
+  const uint16_t* vbase = a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128;
+  const int n_kt = (key_end - key_begin + kKT - 1) / kKT;
+  {
+    Stage st;
+    stage_load(st, kbase, vbase, key_begin, a.T, tid);
+    stage_store(st, Ks[0], Vs[0], tid);
+    if (n_kt > 1) {
+      stage_load(st, kbase, vbase, key_begin + kKT, a.T, tid);
+      stage_store(st, Ks[1], Vs[1], tid);
+    }
+  }
 
   bf16x8 qb[8];
   if (valid) {
@@ -220,102 +225,128 @@ __global__ __launch_bounds__(256) void sel_attn_mfma(const AttnArgs a) {
     for (int s = 0; s < 8; ++s) qb[s] = bf16x8{};
   }
 
-  const uint16_t* kbase = a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128;
-  const uint16_t* vbase = a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128;
+  // per-lane LDS offsets of the MFMA operands
+  int koff[8];  // K: row q, chunk 2s + hi  (row 32 + q has the same swizzle)
+#pragma unroll
+  for (int s = 0; s < 8; ++s) koff[s] = q * kRow + 16 * ((2 * s + hi) ^ (q & 15));
+  const int L = lane & 15, dh = (lane >> 4) & 1;
+  int voff[4];  // V transposing reads: rows 4hi + L/4 (+16ks, +8), dims 32d + 16dh + 4(L%4)
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+    voff[d] = (4 * hi + (L >> 2)) * kRow + 16 * ((4 * d + 2 * dh + ((L & 3) >> 1)) ^ ((L >> 2) << 2)) + 8 * (L & 1);
 
   f32x16 o[4];
 #pragma unroll
   for (int d = 0; d < 4; ++d) o[d] = f32x16{};
   float m_use = -INFINITY, l_run = 0.f;
   const float sc = a.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  const int n_kt = (key_end - key_begin + kKT - 1) / kKT;
-  {
-    TileRegs r;
-    load_tile(r, kbase, vbase, key_begin, a.T, tid);
-    store_tile(r, Ks[0], Vt[0], tid);
-  }
-  __syncthreads();
+  // S^T = K Q^T for the tile in LDS buffer B
+  auto qk = [&](auto B, f32x16& s0, f32x16& s1) {
+    const char* K = Ks[decltype(B)::value];
+    s0 = f32x16{};
+    s1 = f32x16{};
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const bf16x8 k0 = *(const bf16x8*)(K + koff[s]);
+      const bf16x8 k1 = *(const bf16x8*)(K + 32 * kRow + koff[s]);
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], s1, 0, 0, 0);
+    }
+  };
 
-  for (int it = 0; it < n_kt; ++it) {
-    const int kt = key_begin + it * kKT;
-    const int buf = it & 1;
-    const bool has_next = it + 1 < n_kt;
-    TileRegs nx;
-    if (has_next) load_tile(nx, kbase, vbase, kt + kKT, a.T, tid);
-
-    if (kt <= g_wmax) {  // some row of this wavefront sees keys of the tile
-      const uint16_t* K = Ks[buf];
-      const uint16_t* V = Vt[buf];
-      f32x16 s0 = f32x16{}, s1 = f32x16{};
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const bf16x8 k0 = *(const bf16x8*)(K + q * kKPitch + 16 * s + 8 * hi);
-        const bf16x8 k1 = *(const bf16x8*)(K + (32 + q) * kKPitch + 16 * s + 8 * hi);
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], s1, 0, 0, 0);
-      }
-      // causal mask: accumulator register r of block b holds key
-      // kt + 32b + 8(r/4) + 4hi + r%4 for this lane's query
-      if (kt + kKT - 1 > g_wmin) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kt + 8 * (r >> 2) + 4 * hi + (r & 3);
-          if (key > g_q) s0[r] = -INFINITY;
-          if (key + 32 > g_q) s1[r] = -INFINITY;
-        }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-      const float mt = pair_max(mx) * sc;
-      const bool need = mt > m_use + kRescaleLog2;
-      if (__ballot(need)) {
-        const float m_new = need ? mt : m_use;
-        const float alpha = need ? __builtin_amdgcn_exp2f(m_use - m_new) : 1.f;
-        l_run *= alpha;
-#pragma unroll
-        for (int d = 0; d < 4; ++d) o[d] *= alpha;
-        m_use = m_new;
-      }
-      const float msafe = m_use == -INFINITY ? 0.f : m_use;
-      float lsum = 0.f;
-      f32x16 p0, p1;
+  // softmax of the tile starting at key kt, then O^T += V^T P^T from buffer B
+  auto softmax_pv = [&](auto B, int kt, f32x16& s0, f32x16& s1) {
+    const char* V = Vs[decltype(B)::value];
+    // causal mask: accumulator register r of block b holds key
+    // kt + 32b + 8(r/4) + 4hi + r%4 for this lane's query
+    if (kt + kKT - 1 > g_wmin) {
+      const int lim = g_q - kt - 4 * hi;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        p0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], sc, -msafe));
-        p1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], sc, -msafe));
-        lsum += p0[r] + p1[r];
-      }
-      l_run += lsum;
-      bf16x8 pb[4];
-      {
-        typedef float f32x8 __attribute__((ext_vector_type(8)));
-        f32x8 t;
-#pragma unroll
-        for (int x = 0; x < 8; ++x) t[x] = p0[x];
-        pb[0] = __builtin_convertvector(t, bf16x8);
-#pragma unroll
-        for (int x = 0; x < 8; ++x) t[x] = p0[8 + x];
-        pb[1] = __builtin_convertvector(t, bf16x8);
-#pragma unroll
-        for (int x = 0; x < 8; ++x) t[x] = p1[x];
-        pb[2] = __builtin_convertvector(t, bf16x8);
-#pragma unroll
-        for (int x = 0; x < 8; ++x) t[x] = p1[8 + x];
-        pb[3] = __builtin_convertvector(t, bf16x8);
-      }
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          const bf16x8 va = *(const bf16x8*)(V + (32 * d + q) * kVPitch + 16 * ks + 8 * hi);
-          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks], o[d], 0, 0, 0);
-        }
+        const int off = 8 * (r >> 2) + (r & 3);
+        if (off > lim) s0[r] = -INFINITY;
+        if (off + 32 > lim) s1[r] = -INFINITY;
       }
     }
-    if (has_next) store_tile(nx, Ks[buf ^ 1], Vt[buf ^ 1], tid);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+    const float mt = pair_max(mx) * sc;
+    const bool need = mt > m_use + kRescaleLog2;
+    if (__ballot(need)) {
+      const float m_new = need ? mt : m_use;
+      const float alpha = need ? __builtin_amdgcn_exp2f(m_use - m_new) : 1.f;
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) o[d] *= alpha;
+      m_use = m_new;
+    }
+    const float nm = m_use == -INFINITY ? 0.f : -m_use;
+    bf16x8 pb[4];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      pb[0][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s0[x], sc, nm));
+      pb[1][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s0[8 + x], sc, nm));
+      pb[2][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s1[x], sc, nm));
+      pb[3][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s1[8 + x], sc, nm));
+    }
+    // row sum of the bf16 probabilities the PV product uses
+    float lsum = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const bf16x2 pp = {pb[ks][2 * x], pb[ks][2 * x + 1]};
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lsum, false);
+      }
+    l_run += lsum;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const char* vp = V + ks * 16 * kRow + voff[d];
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vp));
+        const bf16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vp + 8 * kRow));
+        const bf16x8 va = __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7);
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks], o[d], 0, 0, 0);
+      }
+    }
+  };
+
+  // One pipeline step: tile i sits in buffer C, tile i+1 in buffer N, tile
+  // i+2 is staged into buffer S (last read two steps ago).  QK^T of tile i+1
+  // is issued before the softmax of tile i so the two overlap.
+  auto step = [&](auto C, auto N, auto S, int i, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
+    const int kt = key_begin + i * kKT;
+    const bool stage = i + 2 < n_kt;
+    Stage st;
+    if (stage) stage_load(st, kbase, vbase, kt + 2 * kKT, a.T, tid);
+    if (i + 1 < n_kt && kt + kKT <= g_wmax) qk(N, n0, n1);
+    if (kt <= g_wmax) softmax_pv(C, kt, c0, c1);
+    if (stage) stage_store(st, Ks[decltype(S)::value], Vs[decltype(S)::value], tid);
     __syncthreads();
+  };
+
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  f32x16 sa0, sa1, sb0, sb1;
+  __syncthreads();
+  if (key_begin <= g_wmax) qk(I0{}, sa0, sa1);
+  for (int i = 0; i < n_kt; i += 6) {
+    step(I0{}, I1{}, I2{}, i, sa0, sa1, sb0, sb1);
+    if (i + 1 >= n_kt) break;
+    step(I1{}, I2{}, I0{}, i + 1, sb0, sb1, sa0, sa1);
+    if (i + 2 >= n_kt) break;
+    step(I2{}, I0{}, I1{}, i + 2, sa0, sa1, sb0, sb1);
+    if (i + 3 >= n_kt) break;
+    step(I0{}, I1{}, I2{}, i + 3, sb0, sb1, sa0, sa1);
+    if (i + 4 >= n_kt) break;
+    step(I1{}, I2{}, I0{}, i + 4, sa0, sa1, sb0, sb1);
+    if (i + 5 >= n_kt) break;
+    step(I2{}, I0{}, I1{}, i + 5, sb0, sb1, sa0, sa1);
   }
 
   const float l_tot = pair_sum(l_run);
@@ -354,12 +385,14 @@ __global__ __launch_bounds__(256) void sel_attn_mfma(const AttnArgs a) {
   }
 }
 
-// Merge the key splits of every multi-split tile.
+// Merge the key splits of every multi-split tile: one block per
+// (tile, KV head, 32 query vectors of one wavefront).
 template <int G>
 __global__ __launch_bounds__(256) void sel_attn_combine(const AttnArgs a) {
   constexpr int RW = 32 / G;
-  constexpr int RT = 4 * RW;
-  const int rest = blockIdx.x;
+  constexpr int RT = kWaves * RW;
+  const int rest = blockIdx.x / kWaves;
+  const int wave = blockIdx.x % kWaves;
   const int kv = rest % a.Hkv;
   const int64_t tile = a.n_tiles - 1 - rest / a.Hkv;
   const int layer = a.lb + blockIdx.y;
@@ -367,12 +400,13 @@ __global__ __launch_bounds__(256) void sel_attn_combine(const AttnArgs a) {
   const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
   const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
   const int ns = (g_last + a.split) / a.split;
-  if (ns <= 1) return;
-  const int64_t items = (int64_t)gridDim.x * a.max_splits;
+  if (ns <= 1 || m0 + wave * RW >= a.n_sel) return;
+  const int64_t items = (int64_t)(gridDim.x / kWaves) * a.max_splits;
   const int64_t slot0 = (int64_t)blockIdx.y * items + (int64_t)rest * a.max_splits;
-  for (int idx = threadIdx.x; idx < kQPerWG * 32; idx += blockDim.x) {
-    const int ql = idx >> 5, d4 = idx & 31;
-    const int wave = ql >> 5, q = ql & 31;
+#pragma unroll 1
+  for (int idx = threadIdx.x; idx < 32 * 32; idx += blockDim.x) {
+    const int q = idx >> 5, d4 = idx & 31;
+    const int ql = wave * 32 + q;
     const int64_t m = m0 + wave * RW + q / G;
     if (m >= a.n_sel) continue;
     const int h = kv * G + q % G;
@@ -381,10 +415,9 @@ __global__ __launch_bounds__(256) void sel_attn_combine(const AttnArgs a) {
     float L = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < ns; ++s) {
-      const float ms = a.part_ml[((slot0 + s) * kQPerWG + ql) * 2];
-      const float ls = a.part_ml[((slot0 + s) * kQPerWG + ql) * 2 + 1];
-      const float w = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M);
-      L += w * ls;
+      const f32x2 ml = *(const f32x2*)(a.part_ml + ((slot0 + s) * kQPerWG + ql) * 2);
+      const float w = ml[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml[0] - M);
+      L += w * ml[1];
       const f32x4 po = *(const f32x4*)(a.part + ((slot0 + s) * kQPerWG + ql) * 128 + 4 * d4);
       acc += w * po;
     }
@@ -507,7 +540,7 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel) {
     p.ws_bytes_per_layer = 0;
     return p;
   }
-  p.rows_per_tile = 4 * (32 / g.G);
+  p.rows_per_tile = kWaves * (32 / g.G);
   p.n_tiles = (n_sel + p.rows_per_tile - 1) / p.rows_per_tile;
   // Spread the key work over about 2048 workgroups per layer.
   const int64_t avg_keys = (g.cs1 + g.T) / 2 + 1;
@@ -525,11 +558,12 @@ template <int G>
 static void launch_mfma_g(const AttnArgs& a, int64_t items, int layers, hipStream_t s) {
   {
     TraceScope tr("sel_attn_mfma", s);
-    hipLaunchKernelGGL(sel_attn_mfma<G>, dim3((unsigned)items, layers), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(sel_attn_mfma<G>, dim3((unsigned)items, layers), dim3(kThreads), 0, s, a);
   }
   if (a.max_splits > 1) {
     TraceScope tr("sel_attn_combine", s);
-    hipLaunchKernelGGL(sel_attn_combine<G>, dim3((unsigned)(a.n_tiles * a.Hkv), layers), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(sel_attn_combine<G>, dim3((unsigned)(a.n_tiles * a.Hkv * kWaves), layers), dim3(256), 0, s,
+                       a);
   }
 }
 
