@@ -143,15 +143,20 @@ struct Stage {
   u32x4 k[2], v[2];
 };
 
-__device__ __forceinline__ void stage_load(Stage& st, const uint16_t* kb, const uint16_t* vb, int kt,
-                                           int64_t T, int tid) {
+// Buffer loads of one K/V plane ([T][128] bf16): rows past the end of the
+// cache read as zeros (hardware range check), and those keys are masked.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const uint16_t* base, int64_t T) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, (int)(T * kRow), 0x00020000);
+}
+
+__device__ __forceinline__ void stage_load(Stage& st, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
+                                           int kt, int tid) {
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int ci = tid + kThreads * j;
-    int key = kt + (ci >> 4);
-    key = key < T ? key : (int)T - 1;  // rows past the cache are masked; keep the address inside it
-    st.k[j] = *(const u32x4*)(kb + (int64_t)key * 128 + 8 * (ci & 15));
-    st.v[j] = *(const u32x4*)(vb + (int64_t)key * 128 + 8 * (ci & 15));
+    const int off = (kt + (ci >> 4)) * kRow + 16 * (ci & 15);
+    st.k[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
+    st.v[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
   }
 }
 
@@ -202,17 +207,15 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   const int g_wmin = mw0 < a.n_sel ? a.sel[mw0] : 0x7fffffff;
   const int g_wmax = mw0 < a.n_sel ? a.sel[mw1] : -1;
 
-  const uint16_t* kbase = a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128;
-  const uint16_t* vbase = a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128;
+  const __amdgpu_buffer_rsrc_t rk = plane_rsrc(a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
+  const __amdgpu_buffer_rsrc_t rv = plane_rsrc(a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
   const int n_kt = (key_end - key_begin + kKT - 1) / kKT;
   {
     Stage st;
-    stage_load(st, kbase, vbase, key_begin, a.T, tid);
+    stage_load(st, rk, rv, key_begin, tid);
     stage_store(st, Ks[0], Vs[0], tid);
-    if (n_kt > 1) {
-      stage_load(st, kbase, vbase, key_begin + kKT, a.T, tid);
-      stage_store(st, Ks[1], Vs[1], tid);
-    }
+    stage_load(st, rk, rv, key_begin + kKT, tid);
+    stage_store(st, Ks[1], Vs[1], tid);
   }
 
   bf16x8 qb[8];
@@ -256,11 +259,10 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     }
   };
 
-  // softmax of the tile starting at key kt, then O^T += V^T P^T from buffer B
-  auto softmax_pv = [&](auto B, int kt, f32x16& s0, f32x16& s1) {
-    const char* V = Vs[decltype(B)::value];
-    // causal mask: accumulator register r of block b holds key
-    // kt + 32b + 8(r/4) + 4hi + r%4 for this lane's query
+  // Causal mask and running max of the tile starting at key kt; rescales the
+  // accumulators when the max grew by more than 2^8.
+  auto mask_max = [&](int kt, f32x16& s0, f32x16& s1) {
+    // accumulator register r of block b holds key kt + 32b + 8(r/4) + 4hi + r%4
     if (kt + kKT - 1 > g_wmin) {
       const int lim = g_q - kt - 4 * hi;
 #pragma unroll
@@ -283,27 +285,32 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
       for (int d = 0; d < 4; ++d) o[d] *= alpha;
       m_use = m_new;
     }
+  };
+
+  // Probabilities of the current tile (buffer C), O^T += V^T P^T, and, in
+  // the same straight-line block, S^T of the next tile (buffer N), so the
+  // exponentials overlap the matrix instructions.
+  auto exp_pv_qk = [&](auto C, auto N, f32x16& s0, f32x16& s1, f32x16& n0, f32x16& n1) {
+    const char* V = Vs[decltype(C)::value];
+    const char* K = Ks[decltype(N)::value];
     const float nm = m_use == -INFINITY ? 0.f : -m_use;
     bf16x8 pb[4];
-#pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      pb[0][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s0[x], sc, nm));
-      pb[1][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s0[8 + x], sc, nm));
-      pb[2][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s1[x], sc, nm));
-      pb[3][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s1[8 + x], sc, nm));
-    }
-    // row sum of the bf16 probabilities the PV product uses
-    float lsum = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const bf16x2 pp = {pb[ks][2 * x], pb[ks][2 * x + 1]};
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lsum, false);
-      }
-    l_run += lsum;
+    n0 = f32x16{};
+    n1 = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
+      const f32x16& sv = ks < 2 ? s0 : s1;
+      const int base = 8 * (ks & 1);
+#pragma unroll
+      for (int x = 0; x < 8; ++x) pb[ks][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sv[base + x], sc, nm));
+      // two k-steps of the next tile's S^T
+#pragma unroll
+      for (int s = 2 * ks; s < 2 * ks + 2; ++s) {
+        const bf16x8 k0 = *(const bf16x8*)(K + koff[s]);
+        const bf16x8 k1 = *(const bf16x8*)(K + 32 * kRow + koff[s]);
+        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
+        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
+      }
 #pragma unroll
       for (int d = 0; d < 4; ++d) {
         const char* vp = V + ks * 16 * kRow + voff[d];
@@ -313,19 +320,32 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
         o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks], o[d], 0, 0, 0);
       }
     }
+    // row sum of the bf16 probabilities the PV product used
+    float lsum = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const bf16x2 pp = {pb[ks][2 * x], pb[ks][2 * x + 1]};
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lsum, false);
+      }
+    l_run += lsum;
   };
 
   // One pipeline step: tile i sits in buffer C, tile i+1 in buffer N, tile
-  // i+2 is staged into buffer S (last read two steps ago).  QK^T of tile i+1
-  // is issued before the softmax of tile i so the two overlap.
+  // i+2 is staged into buffer S (last read two steps ago).  Past the end of
+  // the key range the staged rows are never used and the next-tile product
+  // is discarded, which keeps the step free of branches.  A
+  // wavefront whose rows all end before tile i skips the arithmetic.
   auto step = [&](auto C, auto N, auto S, int i, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
     const int kt = key_begin + i * kKT;
-    const bool stage = i + 2 < n_kt;
     Stage st;
-    if (stage) stage_load(st, kbase, vbase, kt + 2 * kKT, a.T, tid);
-    if (i + 1 < n_kt && kt + kKT <= g_wmax) qk(N, n0, n1);
-    if (kt <= g_wmax) softmax_pv(C, kt, c0, c1);
-    if (stage) stage_store(st, Ks[decltype(S)::value], Vs[decltype(S)::value], tid);
+    stage_load(st, rk, rv, kt + 2 * kKT, tid);
+    if (kt <= g_wmax) {
+      mask_max(kt, c0, c1);
+      exp_pv_qk(C, N, c0, c1, n0, n1);
+    }
+    stage_store(st, Ks[decltype(S)::value], Vs[decltype(S)::value], tid);
     __syncthreads();
   };
 
@@ -334,7 +354,7 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   using I2 = std::integral_constant<int, 2>;
   f32x16 sa0, sa1, sb0, sb1;
   __syncthreads();
-  if (key_begin <= g_wmax) qk(I0{}, sa0, sa1);
+  qk(I0{}, sa0, sa1);
   for (int i = 0; i < n_kt; i += 6) {
     step(I0{}, I1{}, I2{}, i, sa0, sa1, sb0, sb1);
     if (i + 1 >= n_kt) break;
@@ -533,7 +553,8 @@ static int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
 AttnPlan plan_attention(const Geo& g, int64_t n_sel) {
   AttnPlan p{};
-  p.mfma = g.dtype == CS_BF16 && g.D == 128 && g.G <= 32 && 32 % g.G == 0;
+  // (buffer loads address one [T][128] bf16 plane with 32-bit byte offsets)
+  p.mfma = g.dtype == CS_BF16 && g.D == 128 && g.G <= 32 && 32 % g.G == 0 && g.T < (int64_t(1) << 23);
   if (!p.mfma || n_sel == 0) {
     p.split = (int)round_up(g.T, kKT);
     p.max_splits = 1;
