@@ -136,37 +136,42 @@ __device__ __forceinline__ float pair_sum(float x) {
 // of each row permuted so that the operand reads are free of bank conflicts:
 //   K: chunk c of row r sits at position c ^ (r & 15)   (16 rows, same chunk)
 //   V: chunk c of row r sits at position c ^ 4(r & 3)   (4 rows x 4 chunks)
-// A 64-key tile is 2 x 16 KB; each of the 512 threads stages two 16-byte
-// chunks of K and two of V through registers (sixteen consecutive threads
-// read one 256-byte row, so global reads are fully coalesced).
-struct Stage {
-  u32x4 k[2], v[2];
-};
+// A 64-key tile (2 x 16 KB) is staged by buffer->LDS DMA: one wavefront
+// instruction writes 1 KB = 4 rows, lane i landing at byte 16 i, so lane i
+// fetches the global chunk that belongs at its position.  The buffer's
+// hardware range check returns zeros for rows past the cache (those keys are
+// masked).  Each ring slot is its own LDS variable, which lets the compiler
+// see that reads of one slot do not wait for DMA into another.
+typedef __attribute__((address_space(3))) void lds_void;
 
-// Buffer loads of one K/V plane ([T][128] bf16): rows past the end of the
-// cache read as zeros (hardware range check), and those keys are masked.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const uint16_t* base, int64_t T) {
   return __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, (int)(T * kRow), 0x00020000);
 }
 
-__device__ __forceinline__ void stage_load(Stage& st, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
-                                           int kt, int tid) {
+struct StageOffsets {
+  int k[2], v[2];  // byte offset of this lane's chunk within a tile, per instruction
+};
+
+__device__ __forceinline__ StageOffsets stage_offsets(int wave, int lane) {
+  StageOffsets so;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const int ci = tid + kThreads * j;
-    const int off = (kt + (ci >> 4)) * kRow + 16 * (ci & 15);
-    st.k[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
-    st.v[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
+    const int row = 4 * (2 * wave + j) + (lane >> 4);
+    const int p = lane & 15;
+    so.k[j] = row * kRow + 16 * (p ^ (row & 15));
+    so.v[j] = row * kRow + 16 * (p ^ ((row & 3) << 2));
   }
+  return so;
 }
 
-__device__ __forceinline__ void stage_store(const Stage& st, char* Ks, char* Vs, int tid) {
+__device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
+                                          const StageOffsets& so, int kt, char* Kd, char* Vd,
+                                          int wave) {
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const int ci = tid + kThreads * j;
-    const int row = ci >> 4, c = ci & 15;
-    *(u32x4*)(Ks + row * kRow + 16 * (c ^ (row & 15))) = st.k[j];
-    *(u32x4*)(Vs + row * kRow + 16 * (c ^ ((row & 3) << 2))) = st.v[j];
+    const int r0 = 4 * (2 * wave + j);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(Kd + r0 * kRow), 16, kt * kRow + so.k[j], 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(Vd + r0 * kRow), 16, kt * kRow + so.v[j], 0, 0, 0);
   }
 }
 
@@ -174,9 +179,20 @@ template <int G>
 __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   constexpr int RW = 32 / G;       // selected rows per wavefront
   constexpr int RT = kWaves * RW;  // selected rows per workgroup tile
-  constexpr int kBufs = 3;
-  __shared__ __attribute__((aligned(1024))) char Ks[kBufs][kKT * kRow];
-  __shared__ __attribute__((aligned(1024))) char Vs[kBufs][kKT * kRow];
+  __shared__ __attribute__((aligned(1024))) char K0[kKT * kRow], K1[kKT * kRow], K2[kKT * kRow], K3[kKT * kRow];
+  __shared__ __attribute__((aligned(1024))) char V0[kKT * kRow], V1[kKT * kRow], V2[kKT * kRow], V3[kKT * kRow];
+  auto kbuf = [&](auto B) -> char* {
+    if constexpr (decltype(B)::value == 0) return K0;
+    else if constexpr (decltype(B)::value == 1) return K1;
+    else if constexpr (decltype(B)::value == 2) return K2;
+    else return K3;
+  };
+  auto vbuf = [&](auto B) -> char* {
+    if constexpr (decltype(B)::value == 0) return V0;
+    else if constexpr (decltype(B)::value == 1) return V1;
+    else if constexpr (decltype(B)::value == 2) return V2;
+    else return V3;
+  };
 
   const int item = blockIdx.x;
   const int split = item % a.max_splits;
@@ -210,13 +226,10 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   const __amdgpu_buffer_rsrc_t rk = plane_rsrc(a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
   const __amdgpu_buffer_rsrc_t rv = plane_rsrc(a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
   const int n_kt = (key_end - key_begin + kKT - 1) / kKT;
-  {
-    Stage st;
-    stage_load(st, rk, rv, key_begin, tid);
-    stage_store(st, Ks[0], Vs[0], tid);
-    stage_load(st, rk, rv, key_begin + kKT, tid);
-    stage_store(st, Ks[1], Vs[1], tid);
-  }
+  const StageOffsets so = stage_offsets(wave, lane);
+  stage_dma(rk, rv, so, key_begin, K0, V0, wave);
+  stage_dma(rk, rv, so, key_begin + kKT, K1, V1, wave);
+  stage_dma(rk, rv, so, key_begin + 2 * kKT, K2, V2, wave);
 
   bf16x8 qb[8];
   if (valid) {
@@ -247,7 +260,7 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
 
   // S^T = K Q^T for the tile in LDS buffer B
   auto qk = [&](auto B, f32x16& s0, f32x16& s1) {
-    const char* K = Ks[decltype(B)::value];
+    const char* K = kbuf(B);
     s0 = f32x16{};
     s1 = f32x16{};
 #pragma unroll
@@ -288,28 +301,40 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   };
 
   // Probabilities of the current tile (buffer C), O^T += V^T P^T, and, in
-  // the same straight-line block, S^T of the next tile (buffer N), so the
+  // the same straight-line block, k-steps 2..7 of S^T of the next tile
+  // (buffer N; k-steps 0..1 were issued before the running max), so the
   // exponentials overlap the matrix instructions.
-  auto exp_pv_qk = [&](auto C, auto N, f32x16& s0, f32x16& s1, f32x16& n0, f32x16& n1) {
-    const char* V = Vs[decltype(C)::value];
-    const char* K = Ks[decltype(N)::value];
-    const float nm = m_use == -INFINITY ? 0.f : -m_use;
-    bf16x8 pb[4];
+  auto qk_head = [&](auto N, f32x16& n0, f32x16& n1) {
+    const char* K = kbuf(N);
     n0 = f32x16{};
     n1 = f32x16{};
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const bf16x8 k0 = *(const bf16x8*)(K + koff[s]);
+      const bf16x8 k1 = *(const bf16x8*)(K + 32 * kRow + koff[s]);
+      n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
+      n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
+    }
+  };
+  auto exp_pv_qk = [&](auto C, auto N, f32x16& s0, f32x16& s1, f32x16& n0, f32x16& n1) {
+    const char* V = vbuf(C);
+    const char* K = kbuf(N);
+    const float nm = m_use == -INFINITY ? 0.f : -m_use;
+    bf16x8 pb[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const f32x16& sv = ks < 2 ? s0 : s1;
       const int base = 8 * (ks & 1);
 #pragma unroll
       for (int x = 0; x < 8; ++x) pb[ks][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sv[base + x], sc, nm));
-      // two k-steps of the next tile's S^T
+      if (ks < 3) {  // k-steps 2(ks+1), 2(ks+1)+1 of the next tile's S^T
 #pragma unroll
-      for (int s = 2 * ks; s < 2 * ks + 2; ++s) {
-        const bf16x8 k0 = *(const bf16x8*)(K + koff[s]);
-        const bf16x8 k1 = *(const bf16x8*)(K + 32 * kRow + koff[s]);
-        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
-        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
+        for (int s = 2 * ks + 2; s < 2 * ks + 4; ++s) {
+          const bf16x8 k0 = *(const bf16x8*)(K + koff[s]);
+          const bf16x8 k1 = *(const bf16x8*)(K + 32 * kRow + koff[s]);
+          n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
+          n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
+        }
       }
 #pragma unroll
       for (int d = 0; d < 4; ++d) {
@@ -332,42 +357,43 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     l_run += lsum;
   };
 
-  // One pipeline step: tile i sits in buffer C, tile i+1 in buffer N, tile
-  // i+2 is staged into buffer S (last read two steps ago).  Past the end of
-  // the key range the staged rows are never used and the next-tile product
-  // is discarded, which keeps the step free of branches.  A
-  // wavefront whose rows all end before tile i skips the arithmetic.
+  // One pipeline step: tile i sits in ring slot C, tile i+1 in slot N, and
+  // tile i+3 is fetched by DMA into slot S (read last in step i-1).  Each
+  // wavefront then waits only for the DMA of tile i+2 (its four newest
+  // buffer loads, tile i+3's, may stay in flight) before the barrier.  Past
+  // the end of the key range the fetched rows are never used and the
+  // next-tile product is discarded, which keeps the step free of branches.
+  // A wavefront whose rows all end before tile i skips the arithmetic.
   auto step = [&](auto C, auto N, auto S, int i, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
     const int kt = key_begin + i * kKT;
-    Stage st;
-    stage_load(st, rk, rv, kt + 2 * kKT, tid);
+    stage_dma(rk, rv, so, kt + 3 * kKT, kbuf(S), vbuf(S), wave);
     if (kt <= g_wmax) {
+      qk_head(N, n0, n1);
       mask_max(kt, c0, c1);
       exp_pv_qk(C, N, c0, c1, n0, n1);
     }
-    stage_store(st, Ks[decltype(S)::value], Vs[decltype(S)::value], tid);
-    __syncthreads();
+    asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
   };
 
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
   f32x16 sa0, sa1, sb0, sb1;
-  __syncthreads();
+  asm volatile("s_waitcnt vmcnt(4)" ::: "memory");  // tiles 0 and 1 have landed
+  __builtin_amdgcn_s_barrier();
   qk(I0{}, sa0, sa1);
-  for (int i = 0; i < n_kt; i += 6) {
-    step(I0{}, I1{}, I2{}, i, sa0, sa1, sb0, sb1);
+  for (int i = 0; i < n_kt; i += 4) {
+    step(I0{}, I1{}, I3{}, i, sa0, sa1, sb0, sb1);
     if (i + 1 >= n_kt) break;
     step(I1{}, I2{}, I0{}, i + 1, sb0, sb1, sa0, sa1);
     if (i + 2 >= n_kt) break;
-    step(I2{}, I0{}, I1{}, i + 2, sa0, sa1, sb0, sb1);
+    step(I2{}, I3{}, I1{}, i + 2, sa0, sa1, sb0, sb1);
     if (i + 3 >= n_kt) break;
-    step(I0{}, I1{}, I2{}, i + 3, sb0, sb1, sa0, sa1);
-    if (i + 4 >= n_kt) break;
-    step(I1{}, I2{}, I0{}, i + 4, sa0, sa1, sb0, sb1);
-    if (i + 5 >= n_kt) break;
-    step(I2{}, I0{}, I1{}, i + 5, sb0, sb1, sa0, sa1);
+    step(I3{}, I0{}, I2{}, i + 3, sb0, sb1, sa0, sa1);
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // no DMA outlives the workgroup
 
   const float l_tot = pair_sum(l_run);
   // accumulator register r of d-block b holds dim 32b + 8(r/4) + 4hi + r%4
