@@ -285,9 +285,12 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
         if (off + 32 > lim) s1[r] = -INFINITY;
       }
     }
-    float mx = -INFINITY;
+    // balanced max tree (short dependency chain)
+    float t8[8];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+    for (int r = 0; r < 8; ++r) t8[r] = fmaxf(fmaxf(s0[r], s0[r + 8]), fmaxf(s1[r], s1[r + 8]));
+    const float mx = fmaxf(fmaxf(fmaxf(t8[0], t8[1]), fmaxf(t8[2], t8[3])),
+                           fmaxf(fmaxf(t8[4], t8[5]), fmaxf(t8[6], t8[7])));
     const float mt = pair_max(mx) * sc;
     const bool need = mt > m_use + kRescaleLog2;
     if (__ballot(need)) {
