@@ -365,3 +365,35 @@ def test_rebase_large_offsets_all_axes():
     rel = np.sum((got - direct) ** 2) / np.sum(direct ** 2)
     log(f"  rebase8k layer 0 rel-MSE vs direct global rotation: {rel:.2e}")
     assert rel < 2e-5
+
+
+def test_workspace_reuse_and_garbage_workspace():
+    """Split partials live in the caller's workspace: a workspace full of
+    garbage must work, and repeated calls on one workspace must give
+    bit-identical results."""
+    w = ragged(chunk_lens=(1000, 1500, 1700, 800))
+    d = oracle.inputs.build(w)
+    th, sg = theta_sigma(w)
+    k_reb = oracle.rebase.rebase_stored(d["k_stored"], w.dtype, d["chunk_start"], d["chunk_offsets"], th, sg)
+    sc = oracle.score.deviation_f32(dec(k_reb[w.score_layer], w.dtype), dec(d["k_fresh"][w.score_layer], w.dtype), w.cs1)
+    sel = oracle.select.select_top(sc, oracle.select.n_select(0.05, w.n_candidates), w.cs1)
+    b = B()
+    geo = b.Geo.from_workload(w)
+    nbytes = b.selective_attend_scatter_workspace(geo, len(sel), 1)
+    assert nbytes > 0   # this geometry splits its keys
+    ws = torch.full((nbytes,), 0xA5, dtype=torch.uint8, device="cuda")
+    Q, KF, VF = to_dev(d["q_fresh"], w.dtype), to_dev(d["k_fresh"], w.dtype), to_dev(d["v_fresh"], w.dtype)
+    S = torch.from_numpy(sel.astype(np.int32)).cuda()
+    outs = []
+    for rep in range(3):
+        K, V = to_dev(k_reb, w.dtype), to_dev(d["v_stored"], w.dtype)
+        out = empty((w.n_layers, w.n_q_heads, len(sel), w.head_dim), w.dtype)
+        for layer in range(w.n_layers):
+            b.selective_attend_scatter(geo, K, V, layer, layer + 1, S, len(sel), Q, KF, VF, out, None, ws)
+        torch.cuda.synchronize()
+        outs.append(to_host(out, w.dtype))
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+    kp = oracle.attention.scatter_rows(k_reb[0], d["k_fresh"][0], sel, w.cs1)
+    vp = oracle.attention.scatter_rows(d["v_stored"][0], d["v_fresh"][0], sel, w.cs1)
+    o_ref, _ = oracle_attend_layer(w, d, kp, vp, sel, 0)
+    assert rel_l2(dec(outs[0][0], w.dtype), o_ref) <= 1e-2
