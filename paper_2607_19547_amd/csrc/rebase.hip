@@ -41,9 +41,9 @@ __device__ __forceinline__ int axis_of(int i, int sec0, int sec01) {
 }
 
 // ---------------------------------------------------------------- bf16, D = 128
-constexpr int kFastMaxChunks = 96;
-constexpr int kFastTB = 64;  // tokens per workgroup
-constexpr int kFastPG = 8;   // planes (layer x kv head) per workgroup
+constexpr int kFastMaxChunks = 128;
+constexpr int kFastTB = 256;  // tokens per workgroup
+constexpr int kFastPG = 2;   // planes (layer x kv head) per workgroup
 
 struct RebaseFastArgs {
   uint16_t* k;
@@ -73,7 +73,8 @@ __device__ __forceinline__ void rotate8(u32x4& wa, u32x4& wb, const float* c, co
 // Lane layout: 8 lanes per 256-byte row; lane j of the row owns pairs
 // 8j..8j+7, i.e. 16 bytes in each half of the row.  256 threads cover 32 rows
 // per step; a workgroup covers kFastPG planes x kFastTB tokens (16 steps),
-// issuing four steps' loads before any store.
+// issuing four steps' loads before any store.  Loads and stores are
+// non-temporal: every byte is touched exactly once.
 __global__ __launch_bounds__(256) void rebase_bf16_d128(const RebaseFastArgs a) {
   __shared__ float2 tab[64];
   const int c = blockIdx.y;
@@ -111,16 +112,16 @@ __global__ __launch_bounds__(256) void rebase_bf16_d128(const RebaseFastArgs a) 
       ok[u] = plane < a.planes && t0 + tok < len;
       row[u] = a.k + ((int64_t)plane * a.T + base_tok + tok) * 128;
       if (ok[u]) {
-        wa[u] = *(const u32x4*)(row[u] + 8 * j);
-        wb[u] = *(const u32x4*)(row[u] + 64 + 8 * j);
+        wa[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 8 * j));
+        wb[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 64 + 8 * j));
       }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       if (ok[u]) {
         rotate8(wa[u], wb[u], cs_, sn_);
-        *(u32x4*)(row[u] + 8 * j) = wa[u];
-        *(u32x4*)(row[u] + 64 + 8 * j) = wb[u];
+        __builtin_nontemporal_store(wa[u], (u32x4*)(row[u] + 8 * j));
+        __builtin_nontemporal_store(wb[u], (u32x4*)(row[u] + 64 + 8 * j));
       }
     }
   }
