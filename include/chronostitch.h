@@ -167,7 +167,9 @@ cs_status score_deviation_topk(const cs_geometry* g, const void* k_cache,
  *   out            DEVICE [L][H_q][n_sel][D] output, slot order of sel_idx
  *   lse            DEVICE float32 [L][H_q][n_sel] output, or NULL
  *   workspace      DEVICE scratch, >= selective_attend_scatter_workspace()
- *                  for the same n_sel and layer count
+ *                  for the same n_sel and n_layers_per_call >= layer_end -
+ *                  layer_begin (the size grows with the layer count); no
+ *                  initial contents needed, not kept between calls
  * Errors: CS_ERR_INVALID_ARGUMENT, CS_ERR_WORKSPACE_TOO_SMALL, CS_ERR_HIP. */
 cs_status selective_attend_scatter_workspace(const cs_geometry* g, int64_t n_sel,
                                              int32_t n_layers_per_call,

@@ -201,8 +201,10 @@ cs_status selective_attend_scatter_workspace(const cs_geometry* gp, int64_t n_se
   if (n_sel < 0 || n_sel > g.n) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel must be in [0, n]");
   if (n_layers_per_call < 0 || n_layers_per_call > g.L)
     return fail(CS_ERR_INVALID_ARGUMENT, "n_layers_per_call must be in [0, n_layers]");
-  AttnPlan p = plan_attention(g, n_sel);
-  *bytes = p.ws_bytes_per_layer * (size_t)n_layers_per_call;
+  AttnPlan p = plan_attention(g, n_sel, n_layers_per_call);
+  *bytes = n_layers_per_call > 0 && p.mfma && n_sel > 0
+               ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)n_layers_per_call
+               : 0;
   return CS_OK;
 }
 
@@ -220,8 +222,8 @@ cs_status selective_attend_scatter(const cs_geometry* gp, void* k_cache, void* v
   if (n_sel == 0 || layer_end == layer_begin) return CS_OK;
   if (!k_cache || !v_cache || !sel_idx || !q_fresh || !k_fresh || !v_fresh || !out)
     return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
-  AttnPlan p = plan_attention(g, n_sel);
-  size_t need = p.ws_bytes_per_layer * (size_t)(layer_end - layer_begin);
+  AttnPlan p = plan_attention(g, n_sel, layer_end - layer_begin);
+  size_t need = p.mfma ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)(layer_end - layer_begin) : 0;
   if (need && (!workspace || workspace_bytes < need))
     return fail(CS_ERR_WORKSPACE_TOO_SMALL,
                 "workspace smaller than selective_attend_scatter_workspace() (" + std::to_string(need) +

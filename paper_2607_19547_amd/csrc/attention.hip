@@ -3,22 +3,26 @@
 //
 // MFMA path (bf16, head_dim 128, G = H_q/H_kv dividing 32)
 // ---------------------------------------------------------
-// A workgroup owns one KV head, a tile of consecutive selection slots and one
-// key split.  Its 4 wavefronts each hold 32 query vectors: 32/G selected rows
-// x the G query heads that share the KV head, so every K/V tile staged in LDS
-// serves 128 query vectors.  Per 64-key tile a wavefront computes
+// A row tile is one KV head and a run of consecutive selection slots.  Its 8
+// wavefronts each hold 32 query vectors: 32/G selected rows x the G query
+// heads that share the KV head, so every K/V tile staged in LDS serves 256
+// query vectors.  Per 64-key tile a wavefront computes
 //   S^T = K Q^T         (v_mfma_f32_32x32x16_bf16, K from LDS, Q in VGPRs)
 // so each lane ends up holding 32 scores of ONE query; the softmax runs on
 // those registers (exp2 with the 1/sqrt(D) and log2(e) factors folded into one
 // FMA, a lazy running max that rescales only when the max grows by > 2^8),
 // and the probabilities are packed to bf16 directly as the B operand of
-//   O^T += V^T P^T      (V^T from LDS, stored transposed with the key order
-//                        permuted to match the accumulator layout of S^T).
-// K/V tiles are double-buffered in LDS and prefetched into VGPRs one tile
-// ahead.  Rows are causal in cache order: key j is visible to row t iff
-// j <= t; tiles below every row's limit skip the mask.  Long rows are split
-// over the key axis; partial (O, max, sum) go to the workspace and a combine
-// kernel merges them.  Tiles are issued longest first.
+//   O^T += V^T P^T      (V^T read from LDS with transposing loads).
+// K/V tiles reach LDS by buffer->LDS DMA into a 4-slot ring, two tiles ahead
+// of the one being consumed.  Rows are causal in cache order: key j is
+// visible to row t iff j <= t; tiles below every row's limit skip the mask.
+//
+// Work is scheduled through a device-side queue: a planning kernel lists
+// the (row tile, KV head, key piece) items, longest row tiles first, and one
+// persistent workgroup per CU takes items from an atomic counter.  Row tiles
+// too long for an even schedule are cut into key pieces whose partial
+// (O, max, sum) a combine kernel merges in a fixed order, so results do not
+// depend on timing.
 //
 // Generic path: one wavefront per (row, query head), float32 arithmetic, any
 // head_dim <= 512 and either storage dtype.
@@ -112,11 +116,12 @@ struct AttnArgs {
   const int32_t* sel;
   uint16_t* out;
   float* lse;
-  float* part;     // [layers in call][items][kQPerWG][128] partial O (unnormalised)
-  float* part_ml;  // [layers in call][items][kQPerWG][2] running max (log2 units), sum
+  int* plan;       // work plan written by plan_items (see PlanView)
+  float* part;     // [layers in call][part_cap][kQPerWG][128] partial O (unnormalised)
+  float* part_ml;  // [layers in call][part_cap][kQPerWG][2] running max (log2 units), sum
   int64_t T, n, n_sel, n_tiles;
-  int cs1, Hq, Hkv, lb;
-  int split, max_splits;
+  int cs1, Hq, Hkv, lb, layers;
+  int part_cap;      // partial slots per layer
   float scale_log2;  // log2(e) / sqrt(D)
 };
 
@@ -175,6 +180,180 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_bu
   }
 }
 
+// Work decomposition.  Row tiles are ordered longest first (they end at the
+// highest selected tokens); row tile i needs n_i = ceil((g_last + 1) / 64)
+// key tiles.  A row tile longer than the piece size S is cut into
+// ceil(n_i / S) near-equal pieces over its keys.  An item is one piece of one
+// row tile for one KV head.  Items sit in nq queues, queue j holding the KV
+// heads kv = j (mod nq), and the launch places queue j on the XCDs x = j
+// (mod nq), so an XCD's L2 serves few KV heads and every XCD gets the same
+// share of the work.  Within a queue, the pieces of cut row tiles come first,
+// piece-major (piece 0 of every cut row tile, then piece 1, ...: workgroups
+// running side by side read the same keys), then the uncut row tiles, longest
+// first, so each XCD ends with its smallest items.  The pieces of a cut row
+// tile leave partial (O, max, sum) in fixed workspace slots that
+// sel_attn_combine merges in piece order.
+constexpr int kPlanHdr = 16;    // header ints, see PlanView
+constexpr int kPlanCUs = 256;   // CU count S is derived from (a constant: results do not depend on the device)
+constexpr int kItemsPerCU = 8;  // target items per CU when row tiles must be cut
+constexpr int kMinPiece = 16;   // smallest piece: 16 key tiles
+constexpr int kPartCap = 2560;  // partial slots per layer, at most
+constexpr int kXcds = 8;
+
+struct PlanView {
+  int* hdr;   // [8] nq, [9] S, [10] cut row tiles, [11] most pieces, [12] items per queue and layer
+  int* nu;    // [n_tiles] key tiles of row tile i (longest first)
+  int* nsp;   // [n_tiles] pieces of row tile i
+  int* ppre;  // [n_tiles + 1] first partial slot of row tile i (prefix sums of H_kv x pieces over cut row tiles)
+  int* pj;    // [max_pieces + 1] first queue position of piece j (prefix sums of cut row tiles with > j pieces)
+};
+__host__ __device__ inline PlanView plan_view(int* base, int64_t n_tiles) {
+  PlanView v;
+  v.hdr = base;
+  v.nu = base + kPlanHdr;
+  v.nsp = v.nu + n_tiles;
+  v.ppre = v.nsp + n_tiles;
+  v.pj = v.ppre + n_tiles + 1;
+  return v;
+}
+inline size_t plan_ints(int64_t n_tiles, int64_t max_pieces) {
+  return kPlanHdr + 3 * (size_t)n_tiles + 1 + (size_t)max_pieces + 1;
+}
+// Queues: one per KV head (shared by 8/H_kv XCDs), one per XCD, or one.
+__host__ __device__ inline int n_queues(int Hkv) {
+  return Hkv % kXcds == 0 ? kXcds : (kXcds % Hkv == 0 ? Hkv : 1);
+}
+
+// Sum or max over the 1024 threads of the planning workgroup (every thread
+// gets the result).
+__device__ __forceinline__ int block_reduce(int v, bool is_max, int* red) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const int y = __shfl_xor(v, o);
+    v = is_max ? max(v, y) : v + y;
+  }
+  __syncthreads();  // red may still be read by the previous call
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int r = red[0];
+  for (int w = 1; w < 16; ++w) r = is_max ? max(r, red[w]) : r + red[w];
+  return r;
+}
+
+// Inclusive prefix sums of x over the 1024 threads, continuing from *base
+// (shared); returns this thread's inclusive sum and advances *base.
+__device__ __forceinline__ int block_scan(int x, int* wsum, int* base) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  int off = *base;
+  for (int w = 0; w < wave; ++w) off += wsum[w];
+  __syncthreads();
+  if (threadIdx.x == 1023) *base = off + x;
+  __syncthreads();
+  return off + x;
+}
+
+// Builds the work plan of one call (one workgroup of 1024 threads).  Thread t
+// handles row tiles t, t + 1024, ... in every pass, so it reads back only
+// what it wrote itself.
+__global__ __launch_bounds__(1024) void plan_items(const int32_t* __restrict__ sel, int64_t n_sel, int64_t n_tiles,
+                                                   int RT, int64_t T, int Hkv, int part_cap, int* __restrict__ plan) {
+  __shared__ int red[16];
+  __shared__ int wsum[16];
+  __shared__ int s_base;
+  const PlanView pv = plan_view(plan, n_tiles);
+  const int tid = threadIdx.x;
+  int sum = 0, mx = 0;
+  for (int64_t i = tid; i < n_tiles; i += 1024) {
+    const int64_t t = n_tiles - 1 - i;
+    const int64_t ml = min((t + 1) * RT, n_sel) - 1;
+    const int64_t g = min((int64_t)sel[ml], T - 1);
+    const int v = g < 0 ? 1 : (int)((g + kKT) / kKT);
+    pv.nu[i] = v;
+    sum += v;
+    mx = max(mx, v);
+  }
+  const int W1 = block_reduce(sum, false, red);
+  const int nmax = block_reduce(mx, true, red);
+  // piece size: about kItemsPerCU items per CU, raised until the partial
+  // slots fit in part_cap (no cut at all always fits)
+  const int64_t per = (int64_t)kPlanCUs * kItemsPerCU;
+  const int S0 = (int)max<int64_t>(kMinPiece, ((int64_t)W1 * Hkv + per - 1) / per);
+  int S = nmax;
+  if (S0 < nmax) {
+    const int step = max(1, S0 / 8);
+    for (int k = 0; k < 64; ++k) {
+      const int Sk = S0 + k * step;
+      if (Sk >= nmax) break;
+      int loc = 0;
+      for (int64_t i = tid; i < n_tiles; i += 1024) {
+        const int v = pv.nu[i];
+        if (v > Sk) loc += (v + Sk - 1) / Sk;
+      }
+      if ((int64_t)block_reduce(loc, false, red) * Hkv <= part_cap) {
+        S = Sk;
+        break;
+      }
+    }
+  }
+  // pieces per row tile, partial slots of the cut ones
+  int cut = 0, npmax = 1;
+  if (tid == 0) s_base = 0;
+  __syncthreads();
+  for (int64_t b = 0; b < n_tiles; b += 1024) {
+    const int64_t i = b + tid;
+    int np = 1;
+    if (i < n_tiles) {
+      const int v = pv.nu[i];
+      np = v > S ? (v + S - 1) / S : 1;
+      pv.nsp[i] = np;
+      cut += np > 1;
+      npmax = max(npmax, np);
+    }
+    const int inc = block_scan(np > 1 ? np * Hkv : 0, wsum, &s_base);
+    if (i < n_tiles) pv.ppre[i + 1] = inc;
+  }
+  const int n_cut = block_reduce(cut, false, red);
+  const int np_max = block_reduce(npmax, true, red);
+  // queue positions of piece j: (cut row tiles with more than j pieces) x KV heads per queue
+  const int nq = n_queues(Hkv), kvq = Hkv / nq;
+  if (tid == 0) s_base = 0;
+  __syncthreads();
+  const int nj = np_max > 1 ? np_max : 0;
+  for (int b = 0; b < nj; b += 1024) {
+    const int j = b + tid;
+    int c = 0;
+    if (j < nj) {
+      // nsp does not increase along the longest-first order: count by bisection
+      const int need = max(j, 1);  // cut row tiles (nsp > 1) with nsp > j
+      int lo = 0, up = (int)n_tiles;  // first index with nsp <= need
+      while (lo < up) {
+        const int mid = (lo + up) >> 1;
+        if (pv.nsp[mid] > need) lo = mid + 1;
+        else up = mid;
+      }
+      c = lo;
+    }
+    const int inc = block_scan(c * kvq, wsum, &s_base);
+    if (j < nj) pv.pj[j + 1] = inc;
+  }
+  if (tid == 0) {
+    pv.ppre[0] = 0;
+    pv.pj[0] = 0;
+    pv.hdr[8] = nq;
+    pv.hdr[9] = S;
+    pv.hdr[10] = n_cut;
+    pv.hdr[11] = nj;
+    pv.hdr[12] = s_base + (int)(n_tiles - n_cut) * kvq;
+  }
+}
+
 template <int G>
 __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   constexpr int RW = 32 / G;       // selected rows per wavefront
@@ -194,22 +373,68 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     else return V3;
   };
 
-  const int item = blockIdx.x;
-  const int split = item % a.max_splits;
-  const int rest = item / a.max_splits;
-  const int kv = rest % a.Hkv;
-  const int64_t tile = a.n_tiles - 1 - rest / a.Hkv;  // longest rows first
-  const int layer = a.lb + blockIdx.y;
-  const int64_t m0 = tile * RT;
-  const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
-  const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
-  const int key_begin = split * a.split;
-  if (key_begin > g_last) return;  // whole workgroup: this split is past every row
-  const int key_end = min(key_begin + a.split, g_last + 1);
-  const int n_splits_tile = (g_last + a.split) / a.split;
+  const PlanView pv = plan_view(a.plan, a.n_tiles);
+  const int nq = pv.hdr[8], n_cut = pv.hdr[10], nj = pv.hdr[11], per_q = pv.hdr[12];
+  // Workgroup b runs on XCD b mod 8; the XCDs x = j (mod nq) share queue j,
+  // taking its items in turn.
+  const int xs = blockIdx.x % kXcds, share = kXcds / nq;
+  const int jq = xs % nq;
+  const int item = (int)(blockIdx.x / kXcds) * share + xs / nq;
+  if (item >= per_q * a.layers) return;  // whole workgroup: past the end of its queue
+  const int kvq = a.Hkv / nq;
+  const int p_end = pv.pj[nj];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q = lane & 31, hi = lane >> 5;
+  const StageOffsets so = stage_offsets(wave, lane);
+  // per-lane LDS offsets of the MFMA operands
+  int koff[8];  // K: row q, chunk 2s + hi  (row 32 + q has the same swizzle)
+#pragma unroll
+  for (int s = 0; s < 8; ++s) koff[s] = q * kRow + 16 * ((2 * s + hi) ^ (q & 15));
+  const int L = lane & 15, dh = (lane >> 4) & 1;
+  int voff[4];  // V transposing reads: rows 4hi + L/4 (+16ks, +8), dims 32d + 16dh + 4(L%4)
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+    voff[d] = (4 * hi + (L >> 2)) * kRow + 16 * ((4 * d + 2 * dh + ((L & 3) >> 1)) ^ ((L >> 2) << 2)) + 8 * (L & 1);
+  const float sc = a.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  const int lrel = item / per_q;
+  const int r = item - lrel * per_q;
+  int oi, piece, kvl;
+  if (r < p_end) {  // piece j of a cut row tile: pj[j] <= r < pj[j + 1]
+    int lo = 0, up = nj;
+    while (up - lo > 1) {
+      const int mid = (lo + up) >> 1;
+      if (pv.pj[mid] <= r) lo = mid;
+      else up = mid;
+    }
+    const int cnt = (pv.pj[lo + 1] - pv.pj[lo]) / kvq;
+    const int local = r - pv.pj[lo];
+    kvl = local / cnt;
+    oi = local - kvl * cnt;
+    piece = lo;
+  } else {  // an uncut row tile
+    const int nun = (int)a.n_tiles - n_cut;
+    const int local = r - p_end;
+    kvl = local / nun;
+    oi = n_cut + (local - kvl * nun);
+    piece = 0;
+  }
+  const int nsp = pv.nsp[oi], nu = pv.nu[oi];
+  if (piece >= nsp) return;  // (never, for an ascending selection)
+  const int kv = kvl * nq + jq;
+  const int64_t seg_b = (int64_t)piece * nu / nsp, seg_e = (int64_t)(piece + 1) * nu / nsp;
+  const bool full = nsp == 1;
+  const int64_t tile = a.n_tiles - 1 - oi;
+  const int layer = a.lb + lrel;
+
+  const int64_t m0 = tile * RT;
+  const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
+  const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
+  const int key_begin = (int)(seg_b * kKT);
+  const int key_end = min((int)(seg_e * kKT), g_last + 1);
+
   const int64_t m = m0 + wave * RW + q / G;
   const int h = kv * G + q % G;
   int g_q = -1;
@@ -225,8 +450,7 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
 
   const __amdgpu_buffer_rsrc_t rk = plane_rsrc(a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
   const __amdgpu_buffer_rsrc_t rv = plane_rsrc(a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
-  const int n_kt = (key_end - key_begin + kKT - 1) / kKT;
-  const StageOffsets so = stage_offsets(wave, lane);
+  const int n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
   stage_dma(rk, rv, so, key_begin, K0, V0, wave);
   stage_dma(rk, rv, so, key_begin + kKT, K1, V1, wave);
   stage_dma(rk, rv, so, key_begin + 2 * kKT, K2, V2, wave);
@@ -241,22 +465,10 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     for (int s = 0; s < 8; ++s) qb[s] = bf16x8{};
   }
 
-  // per-lane LDS offsets of the MFMA operands
-  int koff[8];  // K: row q, chunk 2s + hi  (row 32 + q has the same swizzle)
-#pragma unroll
-  for (int s = 0; s < 8; ++s) koff[s] = q * kRow + 16 * ((2 * s + hi) ^ (q & 15));
-  const int L = lane & 15, dh = (lane >> 4) & 1;
-  int voff[4];  // V transposing reads: rows 4hi + L/4 (+16ks, +8), dims 32d + 16dh + 4(L%4)
-#pragma unroll
-  for (int d = 0; d < 4; ++d)
-    voff[d] = (4 * hi + (L >> 2)) * kRow + 16 * ((4 * d + 2 * dh + ((L & 3) >> 1)) ^ ((L >> 2) << 2)) + 8 * (L & 1);
-
   f32x16 o[4];
 #pragma unroll
   for (int d = 0; d < 4; ++d) o[d] = f32x16{};
   float m_use = -INFINITY, l_run = 0.f;
-  const float sc = a.scale_log2;
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
   // S^T = K Q^T for the tile in LDS buffer B
   auto qk = [&](auto B, f32x16& s0, f32x16& s1) {
@@ -279,16 +491,16 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     if (kt + kKT - 1 > g_wmin) {
       const int lim = g_q - kt - 4 * hi;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int off = 8 * (r >> 2) + (r & 3);
-        if (off > lim) s0[r] = -INFINITY;
-        if (off + 32 > lim) s1[r] = -INFINITY;
+      for (int rr = 0; rr < 16; ++rr) {
+        const int off = 8 * (rr >> 2) + (rr & 3);
+        if (off > lim) s0[rr] = -INFINITY;
+        if (off + 32 > lim) s1[rr] = -INFINITY;
       }
     }
     // balanced max tree (short dependency chain)
     float t8[8];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) t8[r] = fmaxf(fmaxf(s0[r], s0[r + 8]), fmaxf(s1[r], s1[r + 8]));
+    for (int rr = 0; rr < 8; ++rr) t8[rr] = fmaxf(fmaxf(s0[rr], s0[rr + 8]), fmaxf(s1[rr], s1[rr + 8]));
     const float mx = fmaxf(fmaxf(fmaxf(t8[0], t8[1]), fmaxf(t8[2], t8[3])),
                            fmaxf(fmaxf(t8[4], t8[5]), fmaxf(t8[6], t8[7])));
     const float mt = pair_max(mx) * sc;
@@ -396,28 +608,30 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     if (i + 3 >= n_kt) break;
     step(I3{}, I0{}, I2{}, i + 3, sb0, sb1, sa0, sa1);
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // no DMA outlives the workgroup
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this segment's DMA is complete
+  __builtin_amdgcn_s_barrier();                     // and every wavefront is done with the ring
 
   const float l_tot = pair_sum(l_run);
   // accumulator register r of d-block b holds dim 32b + 8(r/4) + 4hi + r%4
-  if (n_splits_tile == 1) {
-    if (!valid) return;
-    const float inv = 1.f / l_tot;
-    uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128;
+  if (full) {
+    if (valid) {
+      const float inv = 1.f / l_tot;
+      uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128;
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
+      for (int d = 0; d < 4; ++d)
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        u32x2 w;
-        w[0] = pack_bf16x2(o[d][4 * rq] * inv, o[d][4 * rq + 1] * inv);
-        w[1] = pack_bf16x2(o[d][4 * rq + 2] * inv, o[d][4 * rq + 3] * inv);
-        *(u32x2*)(op + 32 * d + 8 * rq + 4 * hi) = w;
-      }
-    if (a.lse && hi == 0)
-      a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (m_use + __log2f(l_tot)) * kLn2;
+        for (int rq = 0; rq < 4; ++rq) {
+          u32x2 w;
+          w[0] = pack_bf16x2(o[d][4 * rq] * inv, o[d][4 * rq + 1] * inv);
+          w[1] = pack_bf16x2(o[d][4 * rq + 2] * inv, o[d][4 * rq + 3] * inv);
+          *(u32x2*)(op + 32 * d + 8 * rq + 4 * hi) = w;
+        }
+      if (a.lse && hi == 0)
+        a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (m_use + __log2f(l_tot)) * kLn2;
+    }
   } else {
     const int ql = wave * 32 + q;
-    const int64_t slot = (int64_t)blockIdx.y * gridDim.x + item;
+    const int64_t slot = (int64_t)lrel * a.part_cap + pv.ppre[oi] + kv * nsp + piece;  // < part_cap per layer
     float* pp = a.part + (slot * kQPerWG + ql) * 128;
 #pragma unroll
     for (int d = 0; d < 4; ++d)
@@ -432,51 +646,50 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
       ml[1] = l_tot;
     }
   }
+
 }
 
-// Merge the key splits of every multi-split tile: one block per
-// (tile, KV head, 32 query vectors of one wavefront).
+// Merge the pieces of every cut row tile, in piece order: one block per
+// (row tile, KV head, wavefront's 32 query vectors) of each layer.
 template <int G>
 __global__ __launch_bounds__(256) void sel_attn_combine(const AttnArgs a) {
   constexpr int RW = 32 / G;
   constexpr int RT = kWaves * RW;
-  const int rest = blockIdx.x / kWaves;
-  const int wave = blockIdx.x % kWaves;
-  const int kv = rest % a.Hkv;
-  const int64_t tile = a.n_tiles - 1 - rest / a.Hkv;
+  const PlanView pv = plan_view(a.plan, a.n_tiles);
+  const int w = blockIdx.x % kWaves;
+  const int kvh = (blockIdx.x / kWaves) % a.Hkv;
+  const int64_t oi = blockIdx.x / (kWaves * a.Hkv);  // longest-first order
+  const int nsp = pv.nsp[oi];
+  if (nsp == 1) return;  // not cut: written directly
   const int layer = a.lb + blockIdx.y;
-  const int64_t m0 = tile * RT;
-  const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
-  const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
-  const int ns = (g_last + a.split) / a.split;
-  if (ns <= 1 || m0 + wave * RW >= a.n_sel) return;
-  const int64_t items = (int64_t)(gridDim.x / kWaves) * a.max_splits;
-  const int64_t slot0 = (int64_t)blockIdx.y * items + (int64_t)rest * a.max_splits;
-#pragma unroll 1
+  const int64_t slot0 = (int64_t)blockIdx.y * a.part_cap + pv.ppre[oi] + kvh * nsp;
+  const int64_t m0 = (a.n_tiles - 1 - oi) * RT;
   for (int idx = threadIdx.x; idx < 32 * 32; idx += blockDim.x) {
-    const int q = idx >> 5, d4 = idx & 31;
-    const int ql = wave * 32 + q;
-    const int64_t m = m0 + wave * RW + q / G;
+    const int qv = 32 * w + (idx >> 5), d4 = idx & 31;  // query vector qv of the tile: row qv / G, head qv % G
+    const int64_t m = m0 + qv / G;
     if (m >= a.n_sel) continue;
-    const int h = kv * G + q % G;
+    const int t = a.sel[m];
+    if (t < a.cs1 || t >= a.T) continue;  // not a later-chunk token: no output (as in the direct path)
+    const int h = kvh * G + qv % G;
     float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, a.part_ml[((slot0 + s) * kQPerWG + ql) * 2]);
-    float L = 0.f;
+    for (int p = 0; p < nsp; ++p) M = fmaxf(M, a.part_ml[((slot0 + p) * kQPerWG + qv) * 2]);
+    float Lsum = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < ns; ++s) {
-      const f32x2 ml = *(const f32x2*)(a.part_ml + ((slot0 + s) * kQPerWG + ql) * 2);
-      const float w = ml[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml[0] - M);
-      L += w * ml[1];
-      const f32x4 po = *(const f32x4*)(a.part + ((slot0 + s) * kQPerWG + ql) * 128 + 4 * d4);
-      acc += w * po;
+    for (int p = 0; p < nsp; ++p) {
+      const int64_t slot = slot0 + p;
+      const f32x2 ml = *(const f32x2*)(a.part_ml + (slot * kQPerWG + qv) * 2);
+      const float wgt = ml[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml[0] - M);
+      Lsum += wgt * ml[1];
+      const f32x4 po = *(const f32x4*)(a.part + (slot * kQPerWG + qv) * 128 + 4 * d4);
+      acc += wgt * po;
     }
-    const float inv = 1.f / L;
+    const float inv = 1.f / Lsum;
     uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128 + 4 * d4;
     u32x2 w2;
     w2[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
     w2[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
     *(u32x2*)op = w2;
-    if (a.lse && d4 == 0) a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (M + __log2f(L)) * kLn2;
+    if (a.lse && d4 == 0) a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (M + __log2f(Lsum)) * kLn2;
   }
 }
 
@@ -580,40 +793,59 @@ __global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a) {
 // ============================================================== planning & launch
 static int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
-AttnPlan plan_attention(const Geo& g, int64_t n_sel) {
+AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call) {
   AttnPlan p{};
-  // (buffer loads address one [T][128] bf16 plane with 32-bit byte offsets)
-  p.mfma = g.dtype == CS_BF16 && g.D == 128 && g.G <= 32 && 32 % g.G == 0 && g.T < (int64_t(1) << 23);
+  // (buffer loads address one [T][128] bf16 plane, plus three tiles of
+  // look-ahead, with 32-bit byte offsets)
+  p.mfma = g.dtype == CS_BF16 && g.D == 128 && g.G <= 32 && 32 % g.G == 0 && g.T <= (int64_t(1) << 23) - 256;
   if (!p.mfma || n_sel == 0) {
-    p.split = (int)round_up(g.T, kKT);
-    p.max_splits = 1;
     p.ws_bytes_per_layer = 0;
+    p.ws_fixed_bytes = 0;
     return p;
   }
   p.rows_per_tile = kWaves * (32 / g.G);
   p.n_tiles = (n_sel + p.rows_per_tile - 1) / p.rows_per_tile;
-  // Spread the key work over about 2048 workgroups per layer.
-  const int64_t avg_keys = (g.cs1 + g.T) / 2 + 1;
-  const int64_t est = p.n_tiles * g.Hkv * avg_keys;
-  int64_t split = round_up(std::max<int64_t>(1024, (est + 2047) / 2048), kKT);
-  if (split >= g.T) split = round_up(g.T, kKT);
-  p.split = (int)split;
-  p.max_splits = (int)((g.T + split - 1) / split);
-  p.ws_bytes_per_layer =
-      p.max_splits > 1 ? (size_t)p.n_tiles * g.Hkv * p.max_splits * kQPerWG * (128 + 2) * sizeof(float) : 0;
+  // Partial slots: a piece has at least kMinPiece key tiles, so a row tile
+  // has at most ceil(ceil(T / 64) / kMinPiece) pieces; the plan keeps the
+  // total under kPartCap per layer by enlarging the pieces.
+  const int64_t max_pieces = ((g.T + kKT - 1) / kKT + kMinPiece - 1) / kMinPiece;
+  // the plan counts key tiles of a layer, and items of a call, in 32-bit integers
+  if (p.n_tiles * ((g.T + kKT - 1) / kKT) * g.Hkv >= (int64_t(1) << 31) ||
+      p.n_tiles * g.Hkv * std::max<int64_t>(1, max_pieces) * std::max(1, layers_per_call) >= (int64_t(1) << 31)) {
+    p.mfma = false;
+    p.ws_bytes_per_layer = 0;
+    p.ws_fixed_bytes = 0;
+    return p;
+  }
+  p.part_cap = (int)std::min<int64_t>(kPartCap, p.n_tiles * g.Hkv * (max_pieces > 1 ? max_pieces : 0));
+  p.ws_fixed_bytes = (plan_ints(p.n_tiles, max_pieces) * sizeof(int) + 255) / 256 * 256;
+  p.ws_bytes_per_layer = (size_t)p.part_cap * kQPerWG * (128 + 2) * sizeof(float);
   return p;
 }
 
 template <int G>
-static void launch_mfma_g(const AttnArgs& a, int64_t items, int layers, hipStream_t s) {
+static void launch_mfma_g(const AttnArgs& a, hipStream_t s) {
+  {
+    TraceScope tr("plan_items", s);
+    hipLaunchKernelGGL(plan_items, dim3(1), dim3(1024), 0, s, a.sel, a.n_sel, a.n_tiles, kWaves * (32 / G), a.T,
+                       a.Hkv, a.part_cap, a.plan);
+  }
   {
     TraceScope tr("sel_attn_mfma", s);
-    hipLaunchKernelGGL(sel_attn_mfma<G>, dim3((unsigned)items, layers), dim3(kThreads), 0, s, a);
+    // items per queue and layer: at most one per row tile and KV head of the
+    // queue, plus the extra pieces of cut row tiles (bounded by part_cap)
+    const int nq = n_queues(a.Hkv);
+    const int64_t per_q = (a.n_tiles * a.Hkv + a.part_cap + nq - 1) / nq;
+    const int64_t share = kXcds / nq;
+    const int64_t grid = (per_q * a.layers + share - 1) / share * kXcds;
+    hipLaunchKernelGGL(sel_attn_mfma<G>, dim3((unsigned)grid), dim3(kThreads), 0, s, a);
   }
-  if (a.max_splits > 1) {
+  if (a.part_cap > 0) {
+    // cut row tiles lead the longest-first order, and each fills at least
+    // 2 H_kv partial slots
+    const int64_t cut_max = std::min<int64_t>(a.n_tiles, a.part_cap / (2 * a.Hkv));
     TraceScope tr("sel_attn_combine", s);
-    hipLaunchKernelGGL(sel_attn_combine<G>, dim3((unsigned)(a.n_tiles * a.Hkv * kWaves), layers), dim3(256), 0, s,
-                       a);
+    hipLaunchKernelGGL(sel_attn_combine<G>, dim3((unsigned)(cut_max * a.Hkv * kWaves), a.layers), dim3(256), 0, s, a);
   }
 }
 
@@ -629,9 +861,9 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const
     a.sel = sel;
     a.out = (uint16_t*)out;
     a.lse = lse;
-    const int64_t items = p.n_tiles * g.Hkv * p.max_splits;
-    a.part = (float*)ws;
-    a.part_ml = a.part ? a.part + (size_t)layers * items * kQPerWG * 128 : nullptr;
+    a.plan = (int*)ws;
+    a.part = (float*)((char*)ws + p.ws_fixed_bytes);
+    a.part_ml = a.part + (size_t)layers * p.part_cap * kQPerWG * 128;
     a.T = g.T;
     a.n = g.n;
     a.n_sel = n_sel;
@@ -640,16 +872,16 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const
     a.Hq = g.Hq;
     a.Hkv = g.Hkv;
     a.lb = lb;
-    a.split = p.split;
-    a.max_splits = p.max_splits;
+    a.layers = layers;
+    a.part_cap = p.part_cap;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g.D));
     switch (g.G) {
-      case 1: launch_mfma_g<1>(a, items, layers, s); break;
-      case 2: launch_mfma_g<2>(a, items, layers, s); break;
-      case 4: launch_mfma_g<4>(a, items, layers, s); break;
-      case 8: launch_mfma_g<8>(a, items, layers, s); break;
-      case 16: launch_mfma_g<16>(a, items, layers, s); break;
-      case 32: launch_mfma_g<32>(a, items, layers, s); break;
+      case 1: launch_mfma_g<1>(a, s); break;
+      case 2: launch_mfma_g<2>(a, s); break;
+      case 4: launch_mfma_g<4>(a, s); break;
+      case 8: launch_mfma_g<8>(a, s); break;
+      case 16: launch_mfma_g<16>(a, s); break;
+      case 32: launch_mfma_g<32>(a, s); break;
       default: return fail(CS_ERR_UNSUPPORTED, "MFMA attention needs H_q/H_kv dividing 32");
     }
     return check_launch("selective attention launch");

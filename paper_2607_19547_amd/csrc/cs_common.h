@@ -76,11 +76,11 @@ struct AttnPlan {
   bool mfma;            // bf16, D = 128, 32 % G == 0
   int rows_per_tile;    // selected rows per workgroup tile
   int64_t n_tiles;      // per KV head
-  int split;            // keys per split (multiple of 64)
-  int max_splits;       // splits of the longest tile
-  size_t ws_bytes_per_layer;
+  int part_cap;         // partial slots per layer
+  size_t ws_fixed_bytes;      // per call: tile plan
+  size_t ws_bytes_per_layer;  // per layer in the call: partial segments
 };
-AttnPlan plan_attention(const Geo& g, int64_t n_sel);
+AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call);
 cs_status launch_attention(const Geo& g, const AttnPlan& plan, const void* k, const void* v,
                            int lb, int le, const int32_t* sel, int64_t n_sel, const void* qf,
                            void* out, float* lse, void* ws, hipStream_t s);

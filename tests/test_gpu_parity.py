@@ -287,7 +287,7 @@ def ragged(n_layers=2, chunk_lens=(100, 130, 103, 167), G=8, Hkv=2, offsets="ran
     (4, 1, (500, 260, 333), 0.2),
     (16, 1, (70, 190), 0.6),
     (32, 1, (40, 90, 31), 0.45),
-    (8, 2, (1000, 1500, 1700, 800), 0.01),      # long rows, few of them: split keys + combine
+    (8, 2, (1000, 1500, 1700, 800), 0.01),      # long rows, few of them: key pieces + combine
     (8, 2, (1000, 1500, 1700, 800), 0.3),
 ])
 def test_ragged_geometries(G, Hkv, lens, rho):
@@ -368,7 +368,7 @@ def test_rebase_large_offsets_all_axes():
 
 
 def test_workspace_reuse_and_garbage_workspace():
-    """Split partials live in the caller's workspace: a workspace full of
+    """Partial results of cut row tiles live in the caller's workspace: a workspace full of
     garbage must work, and repeated calls on one workspace must give
     bit-identical results."""
     w = ragged(chunk_lens=(1000, 1500, 1700, 800))
@@ -380,7 +380,7 @@ def test_workspace_reuse_and_garbage_workspace():
     b = B()
     geo = b.Geo.from_workload(w)
     nbytes = b.selective_attend_scatter_workspace(geo, len(sel), 1)
-    assert nbytes > 0   # this geometry splits its keys
+    assert nbytes > 0   # this geometry cuts its long row tiles into key pieces
     ws = torch.full((nbytes,), 0xA5, dtype=torch.uint8, device="cuda")
     Q, KF, VF = to_dev(d["q_fresh"], w.dtype), to_dev(d["k_fresh"], w.dtype), to_dev(d["v_fresh"], w.dtype)
     S = torch.from_numpy(sel.astype(np.int32)).cuda()
