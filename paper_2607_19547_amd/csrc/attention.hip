@@ -186,8 +186,12 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_bu
 // ceil(n_i / S) near-equal pieces over its keys.  An item is one piece of one
 // row tile for one KV head.  Items sit in nq queues, queue j holding the KV
 // heads kv = j (mod nq), and the launch places queue j on the XCDs x = j
-// (mod nq), so an XCD's L2 serves few KV heads and every XCD gets the same
-// share of the work.  Within a queue, the pieces of cut row tiles come first,
+// (mod nq), so an XCD's L2 serves few KV heads.  The first 3/4 of every
+// queue is dealt to those XCDs in turn by workgroup position; the rest is
+// handed out through an atomic counter per queue to the workgroups that
+// follow on every XCD (an XCD whose queue is empty takes from the others, and
+// surplus workgroups exit), so XCDs that run faster take more of the tail.
+// Within a queue, the pieces of cut row tiles come first,
 // piece-major (piece 0 of every cut row tile, then piece 1, ...: workgroups
 // running side by side read the same keys), then the uncut row tiles, longest
 // first, so each XCD ends with its smallest items.  The pieces of a cut row
@@ -201,7 +205,8 @@ constexpr int kPartCap = 2560;  // partial slots per layer, at most
 constexpr int kXcds = 8;
 
 struct PlanView {
-  int* hdr;   // [8] nq, [9] S, [10] cut row tiles, [11] most pieces, [12] items per queue and layer
+  int* hdr;   // [0, 8) queue counters, [8] nq, [9] S, [10] cut row tiles, [11] most pieces,
+              // [12] items per queue and layer, [13] workgroup rounds placed by position
   int* nu;    // [n_tiles] key tiles of row tile i (longest first)
   int* nsp;   // [n_tiles] pieces of row tile i
   int* ppre;  // [n_tiles + 1] first partial slot of row tile i (prefix sums of H_kv x pieces over cut row tiles)
@@ -263,7 +268,8 @@ __device__ __forceinline__ int block_scan(int x, int* wsum, int* base) {
 // handles row tiles t, t + 1024, ... in every pass, so it reads back only
 // what it wrote itself.
 __global__ __launch_bounds__(1024) void plan_items(const int32_t* __restrict__ sel, int64_t n_sel, int64_t n_tiles,
-                                                   int RT, int64_t T, int Hkv, int part_cap, int* __restrict__ plan) {
+                                                   int RT, int64_t T, int Hkv, int layers, int part_cap,
+                                                   int* __restrict__ plan) {
   __shared__ int red[16];
   __shared__ int wsum[16];
   __shared__ int s_base;
@@ -344,13 +350,18 @@ __global__ __launch_bounds__(1024) void plan_items(const int32_t* __restrict__ s
     if (j < nj) pv.pj[j + 1] = inc;
   }
   if (tid == 0) {
+    const int per_q = s_base + (int)(n_tiles - n_cut) * kvq;
+    const int share = kXcds / nq;
+    const int rounds = (int)((int64_t)per_q * layers * 3 / 4 / share);  // placed by position
     pv.ppre[0] = 0;
     pv.pj[0] = 0;
+    for (int k = 0; k < kXcds; ++k) pv.hdr[k] = rounds * share;  // first item of the dynamic tail
+    pv.hdr[13] = rounds;
     pv.hdr[8] = nq;
     pv.hdr[9] = S;
     pv.hdr[10] = n_cut;
     pv.hdr[11] = nj;
-    pv.hdr[12] = s_base + (int)(n_tiles - n_cut) * kvq;
+    pv.hdr[12] = per_q;
   }
 }
 
@@ -373,14 +384,36 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     else return V3;
   };
 
+  __shared__ int s_take[2];
   const PlanView pv = plan_view(a.plan, a.n_tiles);
-  const int nq = pv.hdr[8], n_cut = pv.hdr[10], nj = pv.hdr[11], per_q = pv.hdr[12];
-  // Workgroup b runs on XCD b mod 8; the XCDs x = j (mod nq) share queue j,
-  // taking its items in turn.
+  const int nq = pv.hdr[8], n_cut = pv.hdr[10], nj = pv.hdr[11], per_q = pv.hdr[12], rounds = pv.hdr[13];
+  const int total_q = per_q * a.layers;
+  // Workgroup b runs on XCD b mod 8; the XCDs x = j (mod nq) share queue j.
   const int xs = blockIdx.x % kXcds, share = kXcds / nq;
-  const int jq = xs % nq;
-  const int item = (int)(blockIdx.x / kXcds) * share + xs / nq;
-  if (item >= per_q * a.layers) return;  // whole workgroup: past the end of its queue
+  const int kround = blockIdx.x / kXcds;
+  int jq = xs % nq, item;
+  if (kround < rounds) {  // placed: the queue's items in turn
+    item = kround * share + xs / nq;
+  } else {  // the tail: the next item of this XCD's queue, else of another
+    if (threadIdx.x == 0) {
+      int got = -1, j = jq;
+      for (int t = 0; t < nq; ++t) {
+        const int v = atomicAdd(&pv.hdr[j], 1);
+        if (v < total_q) {
+          got = v;
+          break;
+        }
+        j = j + 1 == nq ? 0 : j + 1;
+      }
+      s_take[0] = got;
+      s_take[1] = j;
+    }
+    __syncthreads();
+    item = __builtin_amdgcn_readfirstlane(s_take[0]);
+    jq = __builtin_amdgcn_readfirstlane(s_take[1]);
+    if (item < 0) return;  // whole workgroup: every queue is empty
+  }
+  if (item >= total_q) return;  // (placed rounds never reach past the queue)
   const int kvq = a.Hkv / nq;
   const int p_end = pv.pj[nj];
 
@@ -828,7 +861,7 @@ static void launch_mfma_g(const AttnArgs& a, hipStream_t s) {
   {
     TraceScope tr("plan_items", s);
     hipLaunchKernelGGL(plan_items, dim3(1), dim3(1024), 0, s, a.sel, a.n_sel, a.n_tiles, kWaves * (32 / G), a.T,
-                       a.Hkv, a.part_cap, a.plan);
+                       a.Hkv, a.layers, a.part_cap, a.plan);
   }
   {
     TraceScope tr("sel_attn_mfma", s);
