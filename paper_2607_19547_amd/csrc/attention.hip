@@ -106,6 +106,7 @@ constexpr int kWaves = 8;                // wavefronts per workgroup (2 per SIMD
 constexpr int kThreads = 64 * kWaves;
 constexpr int kQPerWG = 32 * kWaves;     // query vectors per workgroup
 constexpr int kRow = 256;                // bytes of one K/V row (bf16 x 128)
+constexpr int kHiLds = 65536;            // LDS bytes below the K ring (the V ring)
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kRescaleLog2 = 8.0f;     // lazy rescale threshold (max growth 2^8)
 
@@ -369,19 +370,24 @@ template <int G>
 __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   constexpr int RW = 32 / G;       // selected rows per wavefront
   constexpr int RT = kWaves * RW;  // selected rows per workgroup tile
-  __shared__ __attribute__((aligned(1024))) char K0[kKT * kRow], K1[kKT * kRow], K2[kKT * kRow], K3[kKT * kRow];
-  __shared__ __attribute__((aligned(1024))) char V0[kKT * kRow], V1[kKT * kRow], V2[kKT * kRow], V3[kKT * kRow];
+  // The V ring takes the low 64 KB of LDS, where the DS instruction's 16-bit
+  // offset reaches every V operand read; the K ring above is read through
+  // per-lane bases that carry the extra 64 KB (see koff).  LDS variables are
+  // laid out in name order, hence lo_* below up_*.  (Any layout computes the
+  // same; this one saves an address add per operand read.)
+  __shared__ __attribute__((aligned(1024))) char lo_v0[kKT * kRow], lo_v1[kKT * kRow], lo_v2[kKT * kRow], lo_v3[kKT * kRow];
+  __shared__ __attribute__((aligned(1024))) char up_k0[kKT * kRow], up_k1[kKT * kRow], up_k2[kKT * kRow], up_k3[kKT * kRow];
   auto kbuf = [&](auto B) -> char* {
-    if constexpr (decltype(B)::value == 0) return K0;
-    else if constexpr (decltype(B)::value == 1) return K1;
-    else if constexpr (decltype(B)::value == 2) return K2;
-    else return K3;
+    if constexpr (decltype(B)::value == 0) return up_k0;
+    else if constexpr (decltype(B)::value == 1) return up_k1;
+    else if constexpr (decltype(B)::value == 2) return up_k2;
+    else return up_k3;
   };
   auto vbuf = [&](auto B) -> char* {
-    if constexpr (decltype(B)::value == 0) return V0;
-    else if constexpr (decltype(B)::value == 1) return V1;
-    else if constexpr (decltype(B)::value == 2) return V2;
-    else return V3;
+    if constexpr (decltype(B)::value == 0) return lo_v0;
+    else if constexpr (decltype(B)::value == 1) return lo_v1;
+    else if constexpr (decltype(B)::value == 2) return lo_v2;
+    else return lo_v3;
   };
 
   __shared__ int s_take[2];
@@ -417,13 +423,18 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   const int kvq = a.Hkv / nq;
   const int p_end = pv.pj[nj];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q = lane & 31, hi = lane >> 5;
   const StageOffsets so = stage_offsets(wave, lane);
   // per-lane LDS offsets of the MFMA operands
-  int koff[8];  // K: row q, chunk 2s + hi  (row 32 + q has the same swizzle)
+  int koff[8];  // K: row q, chunk 2s + hi  (row 32 + q has the same swizzle), plus kHiLds
 #pragma unroll
-  for (int s = 0; s < 8; ++s) koff[s] = q * kRow + 16 * ((2 * s + hi) ^ (q & 15));
+  for (int s = 0; s < 8; ++s) {
+    koff[s] = q * kRow + 16 * ((2 * s + hi) ^ (q & 15));
+    // opaque to constant folding, so that each read keeps this register as
+    // its base and puts (slot - kHiLds) in the instruction's offset field
+    asm("v_add_u32 %0, 0x10000, %1" : "=v"(koff[s]) : "v"(koff[s]));
+  }
   const int L = lane & 15, dh = (lane >> 4) & 1;
   int voff[4];  // V transposing reads: rows 4hi + L/4 (+16ks, +8), dims 32d + 16dh + 4(L%4)
 #pragma unroll
@@ -484,9 +495,9 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   const __amdgpu_buffer_rsrc_t rk = plane_rsrc(a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
   const __amdgpu_buffer_rsrc_t rv = plane_rsrc(a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
   const int n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
-  stage_dma(rk, rv, so, key_begin, K0, V0, wave);
-  stage_dma(rk, rv, so, key_begin + kKT, K1, V1, wave);
-  stage_dma(rk, rv, so, key_begin + 2 * kKT, K2, V2, wave);
+  stage_dma(rk, rv, so, key_begin, up_k0, lo_v0, wave);
+  stage_dma(rk, rv, so, key_begin + kKT, up_k1, lo_v1, wave);
+  stage_dma(rk, rv, so, key_begin + 2 * kKT, up_k2, lo_v2, wave);
 
   bf16x8 qb[8];
   if (valid) {
@@ -510,8 +521,8 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     s1 = f32x16{};
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
-      const bf16x8 k0 = *(const bf16x8*)(K + koff[s]);
-      const bf16x8 k1 = *(const bf16x8*)(K + 32 * kRow + koff[s]);
+      const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
+      const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
       s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], s0, 0, 0, 0);
       s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], s1, 0, 0, 0);
     }
@@ -558,8 +569,8 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
     n1 = f32x16{};
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      const bf16x8 k0 = *(const bf16x8*)(K + koff[s]);
-      const bf16x8 k1 = *(const bf16x8*)(K + 32 * kRow + koff[s]);
+      const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
+      const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
       n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
       n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
     }
@@ -578,8 +589,8 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
       if (ks < 3) {  // k-steps 2(ks+1), 2(ks+1)+1 of the next tile's S^T
 #pragma unroll
         for (int s = 2 * ks + 2; s < 2 * ks + 4; ++s) {
-          const bf16x8 k0 = *(const bf16x8*)(K + koff[s]);
-          const bf16x8 k1 = *(const bf16x8*)(K + 32 * kRow + koff[s]);
+          const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
+          const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
           n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
           n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
         }
