@@ -118,8 +118,8 @@ struct AttnArgs {
   uint16_t* out;
   float* lse;
   int* plan;       // work plan written by plan_items (see PlanView)
-  float* part;     // [layers in call][part_cap][kQPerWG][128] partial O (unnormalised)
-  float* part_ml;  // [layers in call][part_cap][kQPerWG][2] running max (log2 units), sum
+  uint16_t* part;  // [layers in call][part_cap][kQPerWG][128] partial O / sum / 2^e, fp16
+  float* part_ml;  // [layers in call][part_cap][kQPerWG][4] running max (log2 units), sum, e
   int64_t T, n, n_sel, n_tiles;
   int cs1, Hq, Hkv, lb, layers;
   int part_cap;      // partial slots per layer
@@ -200,7 +200,7 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_bu
 // sel_attn_combine merges in piece order.
 constexpr int kPlanHdr = 16;    // header ints, see PlanView
 constexpr int kPlanCUs = 256;   // CU count S is derived from (a constant: results do not depend on the device)
-constexpr int kItemsPerCU = 8;  // target items per CU when row tiles must be cut
+constexpr int kItemsPerCU = 6;  // target items per CU when row tiles must be cut
 constexpr int kMinPiece = 16;   // smallest piece: 16 key tiles
 constexpr int kPartCap = 2560;  // partial slots per layer, at most
 constexpr int kXcds = 8;
@@ -674,20 +674,32 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
         a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (m_use + __log2f(l_tot)) * kLn2;
     }
   } else {
+    // The piece's output row O / sum, scaled by 2^-e so that its largest
+    // magnitude lies in [0.5, 1), is kept in fp16 (11 significant bits,
+    // finer than the bf16 result; the scale keeps the bf16 range of V within
+    // fp16's).
     const int ql = wave * 32 + q;
     const int64_t slot = (int64_t)lrel * a.part_cap + pv.ppre[oi] + kv * nsp + piece;  // < part_cap per layer
-    float* pp = a.part + (slot * kQPerWG + ql) * 128;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    float amax = 0.f;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) amax = fmaxf(amax, fabsf(o[d][r]));
+    amax = pair_max(amax) * inv;
+    const int e = amax > 0.f ? min(max(__builtin_amdgcn_frexp_expf(amax), -100), 100) : 0;  // 2^-e stays normal
+    const float sc_e = inv * __builtin_ldexpf(1.f, -e);
+    uint16_t* pp = a.part + (slot * kQPerWG + ql) * 128;
 #pragma unroll
     for (int d = 0; d < 4; ++d)
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
-        f32x4 w = {o[d][4 * rq], o[d][4 * rq + 1], o[d][4 * rq + 2], o[d][4 * rq + 3]};
-        *(f32x4*)(pp + 32 * d + 8 * rq + 4 * hi) = w;
+        const f32x4 v4 = {o[d][4 * rq] * sc_e, o[d][4 * rq + 1] * sc_e, o[d][4 * rq + 2] * sc_e, o[d][4 * rq + 3] * sc_e};
+        *(f16x4*)(pp + 32 * d + 8 * rq + 4 * hi) = __builtin_convertvector(v4, f16x4);
       }
     if (hi == 0) {
-      float* ml = a.part_ml + (slot * kQPerWG + ql) * 2;
-      ml[0] = m_use;
-      ml[1] = l_tot;
+      const f32x4 ml = {m_use, l_tot, (float)e, 0.f};
+      *(f32x4*)(a.part_ml + (slot * kQPerWG + ql) * 4) = ml;
     }
   }
 
@@ -716,16 +728,16 @@ __global__ __launch_bounds__(256) void sel_attn_combine(const AttnArgs a) {
     if (t < a.cs1 || t >= a.T) continue;  // not a later-chunk token: no output (as in the direct path)
     const int h = kvh * G + qv % G;
     float M = -INFINITY;
-    for (int p = 0; p < nsp; ++p) M = fmaxf(M, a.part_ml[((slot0 + p) * kQPerWG + qv) * 2]);
+    for (int p = 0; p < nsp; ++p) M = fmaxf(M, a.part_ml[((slot0 + p) * kQPerWG + qv) * 4]);
     float Lsum = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int p = 0; p < nsp; ++p) {
       const int64_t slot = slot0 + p;
-      const f32x2 ml = *(const f32x2*)(a.part_ml + (slot * kQPerWG + qv) * 2);
-      const float wgt = ml[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml[0] - M);
-      Lsum += wgt * ml[1];
-      const f32x4 po = *(const f32x4*)(a.part + (slot * kQPerWG + qv) * 128 + 4 * d4);
-      acc += wgt * po;
+      const f32x4 ml = *(const f32x4*)(a.part_ml + (slot * kQPerWG + qv) * 4);
+      const float wgt = ml[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml[0] - M) * ml[1];
+      Lsum += wgt;
+      const f16x4 po = *(const f16x4*)(a.part + (slot * kQPerWG + qv) * 128 + 4 * d4);
+      acc += (wgt * __builtin_ldexpf(1.f, (int)ml[2])) * __builtin_convertvector(po, f32x4);
     }
     const float inv = 1.f / Lsum;
     uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128 + 4 * d4;
@@ -863,7 +875,7 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call) {
   }
   p.part_cap = (int)std::min<int64_t>(kPartCap, p.n_tiles * g.Hkv * (max_pieces > 1 ? max_pieces : 0));
   p.ws_fixed_bytes = (plan_ints(p.n_tiles, max_pieces) * sizeof(int) + 255) / 256 * 256;
-  p.ws_bytes_per_layer = (size_t)p.part_cap * kQPerWG * (128 + 2) * sizeof(float);
+  p.ws_bytes_per_layer = (size_t)p.part_cap * kQPerWG * (128 * sizeof(uint16_t) + 4 * sizeof(float));
   return p;
 }
 
@@ -906,8 +918,8 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const
     a.out = (uint16_t*)out;
     a.lse = lse;
     a.plan = (int*)ws;
-    a.part = (float*)((char*)ws + p.ws_fixed_bytes);
-    a.part_ml = a.part + (size_t)layers * p.part_cap * kQPerWG * 128;
+    a.part = (uint16_t*)((char*)ws + p.ws_fixed_bytes);
+    a.part_ml = (float*)(a.part + (size_t)layers * p.part_cap * kQPerWG * 128);
     a.T = g.T;
     a.n = g.n;
     a.n_sel = n_sel;
