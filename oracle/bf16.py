@@ -13,6 +13,7 @@ import numpy as np
 
 _EXP_MIN = -126          # smallest normal exponent of bfloat16 (same as float32)
 _MANT_BITS = 7           # stored significand bits
+_CHUNK = 1 << 16         # elements per slice in encode
 
 
 def decode(bits):
@@ -32,6 +33,12 @@ def encode(x):
     is the answer.  The exponent e is read from the float64 bit pattern.
     """
     x = np.asarray(x, dtype=np.float64)
+    if x.size > _CHUNK:  # elementwise: the same steps, one cache-sized slice at a time
+        flat = x.reshape(-1)
+        out = np.empty(flat.shape, dtype=np.uint16)
+        for i in range(0, flat.size, _CHUNK):
+            out[i:i + _CHUNK] = encode(flat[i:i + _CHUNK])
+        return out.reshape(x.shape)
     a = np.abs(x)
     ebits = (a.view(np.uint64) >> np.uint64(52)).astype(np.int64)   # biased exponent
     lead = np.where(ebits == 0, -1075, ebits - 1023)                 # fp64 subnormals: far below bf16 range

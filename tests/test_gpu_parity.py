@@ -289,6 +289,9 @@ def ragged(n_layers=2, chunk_lens=(100, 130, 103, 167), G=8, Hkv=2, offsets="ran
     (32, 1, (40, 90, 31), 0.45),
     (8, 2, (1000, 1500, 1700, 800), 0.01),      # long rows, few of them: key pieces + combine
     (8, 2, (1000, 1500, 1700, 800), 0.3),
+    (4, 4, (200, 260, 333), 0.25),              # one queue per KV head on 2 XCDs each
+    (2, 8, (100, 300, 200), 0.3),               # one queue per XCD
+    (1, 16, (64, 200, 150), 0.2),               # two KV heads per queue
 ])
 def test_ragged_geometries(G, Hkv, lens, rho):
     w = ragged(G=G, Hkv=Hkv, chunk_lens=lens)
@@ -397,3 +400,73 @@ def test_workspace_reuse_and_garbage_workspace():
     vp = oracle.attention.scatter_rows(d["v_stored"][0], d["v_fresh"][0], sel, w.cs1)
     o_ref, _ = oracle_attend_layer(w, d, kp, vp, sel, 0)
     assert rel_l2(dec(outs[0][0], w.dtype), o_ref) <= 1e-2
+
+
+# ======================================================================== full size, sampled
+def _sample_slots(k, rt, n_random, seed):
+    """Slots at both ends, around row-tile boundaries and at random."""
+    pick = {0, 1, k - 2, k - 1}
+    for b in (rt, 2 * rt, k // 2, k - rt):
+        pick.update({b - 1, b})
+    rng = np.random.default_rng(seed)
+    pick.update(rng.choice(k, size=min(n_random, k), replace=False).tolist())
+    return np.array(sorted(x for x in pick if 0 <= x < k), dtype=np.int64)
+
+
+def _isolated_full_size(w, rhos, n_random, check_rebase):
+    """Stage-isolated checks at full size: every stage's GPU result from the
+    oracle's own inputs.  Rebase: every element; scores: bit-exact on the
+    oracle's rebased keys; selection: exact; scatter: exact; attention: the
+    sampled slots of every layer and head (one call per layer, as timed)."""
+    d = oracle.inputs.build(w, q_layers=[0])
+    th, sg = theta_sigma(w)
+    k_reb = oracle.rebase.rebase_stored(d["k_stored"], w.dtype, d["chunk_start"], d["chunk_offsets"], th, sg)
+    b = B()
+    geo = b.Geo.from_workload(w)
+    if check_rebase:
+        K = to_dev(d["k_stored"], w.dtype)
+        b.compose_rebase_k(geo, K, d["chunk_offsets"])
+        assert_rebase_close(w, to_host(K, w.dtype), k_reb, d["k_stored"])
+        del K
+    n = w.n_candidates
+    ref_scores = oracle.score.deviation_f32(dec(k_reb[w.score_layer], w.dtype),
+                                            dec(d["k_fresh"][w.score_layer], w.dtype), w.cs1)
+    K = to_dev(k_reb, w.dtype)
+    KF = to_dev(d["k_fresh"][w.score_layer], w.dtype)
+    for rho in rhos:
+        scores = torch.empty(n, dtype=torch.float32, device="cuda")
+        sel = torch.empty(n, dtype=torch.int32, device="cuda")
+        k = b.score_deviation_topk(geo, K, w.score_layer, KF, rho, scores, sel)
+        torch.cuda.synchronize()
+        assert k == oracle.select.n_select(rho, n)
+        assert np.array_equal(scores.cpu().numpy(), ref_scores)
+        ref_sel = oracle.select.select_top(ref_scores, k, w.cs1)
+        assert sel[:k].cpu().numpy().tolist() == ref_sel.tolist()
+        kp, vp, out, lse = gpu_attend(w, k_reb, d["v_stored"], d, ref_sel)
+        rt = 8 * (32 // (w.n_q_heads // w.n_kv_heads))
+        slots = _sample_slots(k, rt, n_random, seed=int(rho * 1000) + 1)
+        for layer in range(w.n_layers):
+            kpo = oracle.attention.scatter_rows(k_reb[layer], d["k_fresh"][layer], ref_sel, w.cs1)
+            vpo = oracle.attention.scatter_rows(d["v_stored"][layer], d["v_fresh"][layer], ref_sel, w.cs1)
+            assert np.array_equal(kp[layer], kpo) and np.array_equal(vp[layer], vpo)
+            o_ref, lse_ref = oracle_attend_layer(w, d, kpo, vpo, ref_sel, layer, rows=ref_sel[slots])
+            check_attention(w, out[layer][:, slots], lse[layer][:, slots], o_ref, lse_ref,
+                            f"{w.name} rho={rho} layer {layer}, {len(slots)} sampled slots of {k}")
+
+
+def test_long65k_per_layer_sampled():
+    """The timed configuration: 65536 tokens in 32 chunks of 2048, 16 Q / 2 KV
+    heads, head_dim 128, bf16, one call per layer; its first two layers (the
+    layers are independent and identically shaped), at rho = 0.1 and 1."""
+    w = dataclasses.replace(synth.WORKLOADS["long65k"], n_layers=2)
+    log(f"case long65k first two layers, T={w.n_tokens}")
+    _isolated_full_size(w, rhos=(0.1, 1.0), n_random=48, check_rebase=True)
+
+
+def test_more_than_1024_row_tiles():
+    """G = 32 puts 8 selected rows in a row tile: 9000 selected rows make 1125
+    row tiles, more than the planning workgroup's 1024 threads, with cut row
+    tiles of up to three pieces."""
+    w = ragged(n_layers=1, G=32, Hkv=1, chunk_lens=(64, 9000))
+    log(f"case ragged G=32 Hkv=1 lens=(64, 9000) rho=1")
+    _isolated_full_size(w, rhos=(1.0,), n_random=64, check_rebase=False)
