@@ -42,8 +42,10 @@ __device__ __forceinline__ int axis_of(int i, int sec0, int sec01) {
 
 // ---------------------------------------------------------------- bf16, D = 128
 constexpr int kFastMaxChunks = 128;
-constexpr int kFastTB = 256;  // tokens per workgroup
+constexpr int kFastTB = 64;  // tokens per workgroup
 constexpr int kFastPG = 2;   // planes (layer x kv head) per workgroup
+constexpr int kFastR = (kFastPG * kFastTB) / 32;  // rows per lane group (256 threads = 32 lane groups)
+static_assert((kFastPG * kFastTB) % 32 == 0, "a workgroup covers whole lane-group steps");
 
 struct RebaseFastArgs {
   uint16_t* k;
@@ -51,6 +53,7 @@ struct RebaseFastArgs {
   int planes;
   int sec0, sec01;
   int tblocks;  // token blocks of the longest chunk in this launch
+  int nc;       // chunks in this launch
   double theta[64];
   int start[kFastMaxChunks];
   int len[kFastMaxChunks];
@@ -71,58 +74,58 @@ __device__ __forceinline__ void rotate8(u32x4& wa, u32x4& wb, const float* c, co
 }
 
 // Lane layout: 8 lanes per 256-byte row; lane j of the row owns pairs
-// 8j..8j+7, i.e. 16 bytes in each half of the row.  256 threads cover 32 rows
-// per step; a workgroup covers kFastPG planes x kFastTB tokens (16 steps),
-// issuing four steps' loads before any store.  Loads and stores are
-// non-temporal: every byte is touched exactly once.
+// 8j..8j+7, i.e. 16 bytes in each half of the row.  A workgroup of 256
+// threads covers kFastPG planes x kFastTB tokens of one chunk, one row per
+// lane group and plane-token step, all loads issued (non-temporal: every byte
+// is touched once) before the chunk's table is built, then rotated and
+// stored.  Small workgroups in address order (token block fastest, then
+// chunk, then plane group) keep many independent streams in flight over
+// neighbouring memory.
 __global__ __launch_bounds__(256) void rebase_bf16_d128(const RebaseFastArgs a) {
   __shared__ float2 tab[64];
-  const int c = blockIdx.y;
   const int tb = blockIdx.x % a.tblocks;
-  const int pg = blockIdx.x / a.tblocks;
+  const int c = (blockIdx.x / a.tblocks) % a.nc;
+  const int pg = blockIdx.x / (a.tblocks * a.nc);
   const int len = a.len[c];
   const int t0 = tb * kFastTB;
   if (t0 >= len) return;  // whole workgroup
+  const int j = threadIdx.x & 7;
+  const int r0 = threadIdx.x >> 3;  // 0..31
+  const int64_t base_tok = a.start[c] + t0;
+  u32x4 wa[kFastR], wb[kFastR];
+  uint16_t* row[kFastR];
+  bool ok[kFastR];
+#pragma unroll
+  for (int u = 0; u < kFastR; ++u) {
+    const int idx = u * 32 + r0;
+    const int plane = pg * kFastPG + idx / kFastTB;
+    const int tok = idx % kFastTB;
+    ok[u] = plane < a.planes && t0 + tok < len;
+    row[u] = a.k + ((int64_t)plane * a.T + base_tok + tok) * 128;
+    if (ok[u]) {
+      wa[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 8 * j));
+      wb[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 64 + 8 * j));
+    }
+  }
   if (threadIdx.x < 64) {
     const int i = threadIdx.x;
     const double phi = (double)a.off[c][axis_of(i, a.sec0, a.sec01)] * a.theta[i];
     tab[i] = cos_sin_of(phi);
   }
   __syncthreads();
-  const int j = threadIdx.x & 7;
-  const int r0 = threadIdx.x >> 3;  // 0..31
   float cs_[8], sn_[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    float2 t = tab[8 * j + e];
+    const float2 t = tab[8 * j + e];
     cs_[e] = t.x;
     sn_[e] = t.y;
   }
-  const int64_t base_tok = a.start[c] + t0;
-#pragma unroll 1
-  for (int it = 0; it < (kFastPG * kFastTB) / 32; it += 4) {
-    u32x4 wa[4], wb[4];
-    uint16_t* row[4];
-    bool ok[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int idx = (it + u) * 32 + r0;
-      const int plane = pg * kFastPG + idx / kFastTB;
-      const int tok = idx % kFastTB;
-      ok[u] = plane < a.planes && t0 + tok < len;
-      row[u] = a.k + ((int64_t)plane * a.T + base_tok + tok) * 128;
-      if (ok[u]) {
-        wa[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 8 * j));
-        wb[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 64 + 8 * j));
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (ok[u]) {
-        rotate8(wa[u], wb[u], cs_, sn_);
-        __builtin_nontemporal_store(wa[u], (u32x4*)(row[u] + 8 * j));
-        __builtin_nontemporal_store(wb[u], (u32x4*)(row[u] + 64 + 8 * j));
-      }
+  for (int u = 0; u < kFastR; ++u) {
+    if (ok[u]) {
+      rotate8(wa[u], wb[u], cs_, sn_);
+      __builtin_nontemporal_store(wa[u], (u32x4*)(row[u] + 8 * j));
+      __builtin_nontemporal_store(wb[u], (u32x4*)(row[u] + 64 + 8 * j));
     }
   }
 }
@@ -215,7 +218,8 @@ cs_status launch_rebase(const Geo& g, void* k, const int32_t* off, const double*
       }
       const int pgroups = (planes + kFastPG - 1) / kFastPG;
       TraceScope tr("rebase_bf16_d128", s);
-      hipLaunchKernelGGL(rebase_bf16_d128, dim3(a.tblocks * pgroups, nc), dim3(256), 0, s, a);
+      a.nc = nc;
+      hipLaunchKernelGGL(rebase_bf16_d128, dim3((unsigned)(a.tblocks * pgroups * nc)), dim3(256), 0, s, a);
     } else {
       RebaseGenArgs a;
       a.k = k;
