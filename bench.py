@@ -50,6 +50,11 @@ def parse():
     p.add_argument("--cpu-baseline", type=int, default=1, help="time the CPU oracle on a sample (0: skip)")
     p.add_argument("--batched-layers", type=int, default=0,
                    help="one selective_attend_scatter call over all layers instead of one per layer")
+    p.add_argument("--batched-steps", type=int, default=3,
+                   help="steps also timed with one batched attention call over all layers (0: skip)")
+    p.add_argument("--sweep", choices=("none", "rebase", "attention"), default="none",
+                   help="rebase: 8k/65k/262k-token K caches with and without a cache flush; "
+                        "attention: the 32k-token cache at rho in {0.05, 0.1, 0.2, 0.5, 1}")
     return p.parse_args()
 
 
@@ -112,6 +117,10 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     binding.lib()
+    if args.sweep == "rebase":
+        return sweep_rebase(args, binding, synth, torch)
+    if args.sweep == "attention":
+        return sweep_attention(args, binding, synth, torch)
     w = synth.WORKLOADS[args.workload]
     rho = w.rho if args.rho is None else args.rho
     inp = Inputs(w, torch, binding, synth)
@@ -119,8 +128,11 @@ def main():
     rho1 = None
     if args.rho1_steps > 0 and rho != 1.0:
         rho1 = bench_rho(inp, w, 1.0, args.rho1_steps, 1, binding, torch, bool(args.batched_layers))
+    other = None
+    if args.batched_steps > 0:  # the other launch mode, for comparison
+        other = bench_rho(inp, w, rho, args.batched_steps, 1, binding, torch, not args.batched_layers)
     cpu = cpu_baseline(w, rho) if args.cpu_baseline else None
-    emit(args, w, rho, result, rho1, cpu)
+    emit(args, w, rho, result, rho1, cpu, other)
 
 
 def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched):
@@ -179,6 +191,105 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched):
     return res
 
 
+def _events(torch, stream, fn, reps, before=None):
+    """Median milliseconds of fn() between HIP events on the library's stream."""
+    times = []
+    for _ in range(reps):
+        if before is not None:
+            before()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    return float(np.median(times)), float(np.min(times))
+
+
+def sweep_rebase(args, b, synth, torch):
+    """compose_rebase_k on K caches of 8k, 65k and 262k tokens (2048-token chunks, every chunk moved
+    on all three axes), restored before every repetition; with a flush, 1 GiB of unrelated data is
+    written between the restore and the timed call so that no part of K is still in the caches."""
+    stream = torch.cuda.current_stream()
+    junk = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    rows = []
+    for name in ("rebase8k", "rebase65k", "rebase262k"):
+        w = synth.WORKLOADS[name]
+        geo = b.Geo.from_workload(w)
+        off = synth.chunk_offsets(w)
+        K0 = torch.empty((w.n_layers, w.n_kv_heads, w.n_tokens, w.head_dim), dtype=torch.bfloat16, device="cuda")
+        for layer in range(w.n_layers):
+            K0[layer] = synth.torch_normal((w.n_kv_heads, w.n_tokens, w.head_dim), w.seed, 0, synth.TAG_K, layer,
+                                           "cuda", torch.bfloat16)
+        K = K0.clone()
+        cs = w.chunk_start
+        rot = int(sum(cs[c + 1] - cs[c] for c in range(w.n_chunks) if np.any(off[c])))
+        nbytes = 2 * w.n_layers * w.n_kv_heads * rot * w.head_dim * 2
+        for flush in (True, False):
+            def before(flush=flush):
+                K.copy_(K0)
+                if flush:
+                    junk.fill_(7)
+            med, best = _events(torch, stream, lambda: b.compose_rebase_k(geo, K, off), args.steps + 1, before)
+            gbps = nbytes / (med * 1e-3) / 1e9
+            rows.append({"workload": name, "tokens": w.n_tokens, "bytes": nbytes, "flush": flush,
+                         "ms": round(med, 4), "ms_min": round(best, 4), "GBps": round(gbps, 1),
+                         "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
+            log(f"[bench] {name} flush={flush}: {med * 1e3:.1f} us, {gbps:.1f} GB/s")
+        del K0, K
+    print(json.dumps({"metric": "rebase GB/s (% HBM peak) by cache size", "unit": "GB/s", "n_gpus": 1,
+                      "higher_is_better": True, "dtype": "bf16", "data": "synthetic", "sweep": rows}), flush=True)
+
+
+def sweep_attention(args, b, synth, torch):
+    """The 32k-token cache (16 chunks of 2048, 36 layers): one per-layer scatter + attention call at
+    each rho; TFLOP/s from the algorithmic flops of the selection over the whole stage's kernels."""
+    w = synth.WORKLOADS["attn32k"]
+    inp = Inputs(w, torch, b, synth)
+    n = w.n_candidates
+    stream = torch.cuda.current_stream()
+    rows = []
+    base = None
+    for rho in (1.0, 0.5, 0.2, 0.1, 0.05):
+        inp.K.copy_(inp.K0)  # fresh composition: the selection ranks unscattered rows
+        inp.V.copy_(inp.V0)
+        b.compose_rebase_k(inp.geo, inp.K, inp.offsets)
+        scores = torch.empty(n, dtype=torch.float32, device="cuda")
+        sel = torch.empty(n, dtype=torch.int32, device="cuda")
+        k = b.score_deviation_topk(inp.geo, inp.K, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
+        out = torch.empty((w.n_layers, w.n_q_heads, k, w.head_dim), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty(max(b.selective_attend_scatter_workspace(inp.geo, k, 1), 1), dtype=torch.uint8,
+                         device="cuda")
+        g = sel[:k].cpu().numpy().astype(np.int64)
+        flops = 4 * w.head_dim * w.n_q_heads * int(np.sum(g + 1))   # per layer
+
+        def stage():
+            for layer in range(w.n_layers):
+                b.selective_attend_scatter(inp.geo, inp.K, inp.V, layer, layer + 1, sel, k, inp.QF, inp.KF,
+                                           inp.VF, out, None, ws)
+        stage()  # warm-up
+        b.cs_trace_reset()
+        b.cs_trace_enable(True)
+        med, _ = _events(torch, stream, stage, max(args.steps // 2, 2))
+        b.cs_trace_enable(False)
+        tr = b.cs_trace_collect()
+        an, ams = tr.get("sel_attn_mfma", (1, 0.0))
+        kern_tflops = flops / (ams / an * 1e-3) / 1e12
+        stage_tflops = w.n_layers * flops / (med * 1e-3) / 1e12
+        if base is None:
+            base = med
+        rows.append({"rho": rho, "n_sel": k, "stage_ms": round(med, 3), "flops_per_layer": flops,
+                     "stage_TFLOPs": round(stage_tflops, 1), "kernel_TFLOPs": round(kern_tflops, 1),
+                     "kernel_frac_mfma": round(kern_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "speedup_vs_rho1": round(base / med, 3)})
+        log(f"[bench] attn32k rho={rho}: k={k}, stage {med:.3f} ms, kernel {kern_tflops:.1f} TFLOP/s")
+    print(json.dumps({"metric": "selective attention TFLOP/s (% MFMA peak) by rho, 32k-token cache",
+                      "unit": "TFLOP/s", "n_gpus": 1, "higher_is_better": True, "dtype": "bf16",
+                      "data": "synthetic", "sweep": rows}), flush=True)
+
+
 def cpu_baseline(w, rho):
     """The CPU oracle, as it stands, on a bounded sample of the same workload:
     re-basing and attention of ONE of the 36 layers (the scoring layer) plus the
@@ -234,7 +345,7 @@ def _traffic(kernel):
         return None
 
 
-def emit(args, w, rho, r, rho1, cpu):
+def emit(args, w, rho, r, rho1, cpu, other=None):
     tr = r["trace"]
     steps = r["steps"]
     attn_n, attn_ms = tr.get("sel_attn_mfma", (0, 0.0))
@@ -292,6 +403,8 @@ def emit(args, w, rho, r, rho1, cpu):
             "avg_launch_us": round(reb_avg_s * 1e6, 2),
         },
     }
+    if other is not None:
+        line["per_layer_compose_ms" if args.batched_layers else "batched_compose_ms"] = round(other["ms"], 4)
     if rho1 is not None:
         line["rho1_compose_ms"] = round(rho1["ms"], 3)
         line["rho1_over_rho_speedup"] = round(rho1["ms"] / r["ms"], 3)
