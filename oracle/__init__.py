@@ -22,4 +22,4 @@ Modules
 Every function here is pinned by ``tests/test_oracle_*.py`` against closed
 forms, invariants, library routines or brute force; none is "parity unpinned".
 """
-from . import bf16, rope, rebase, score, select, attention, compose, inputs  # noqa: F401
+from . import bf16, rope, rebase, score, select, attention, compose, inputs, policies  # noqa: F401
