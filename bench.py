@@ -53,7 +53,8 @@ def parse():
     p.add_argument("--batched-steps", type=int, default=3,
                    help="steps also timed with one batched attention call over all layers (0: skip)")
     p.add_argument("--sweep", choices=("none", "rebase", "attention"), default="none",
-                   help="rebase: 8k/65k/262k-token K caches with and without a cache flush; "
+                   help="rebase: 8k/65k/262k-token K caches with and without a cache flush, and the "
+                        "per-token (scalar re-basing) kernel on the 65k cache; "
                         "attention: the 32k-token cache at rho in {0.05, 0.1, 0.2, 0.5, 1}")
     return p.parse_args()
 
@@ -248,6 +249,33 @@ def sweep_rebase(args, b, synth, torch):
                          "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
             log(f"[bench] {name} flush={flush}: {med * 1e3:.1f} us, {gbps:.1f} GB/s")
         del K0, K
+    # per-token offsets: scalar re-basing (token j of the composed cache to (j, j, j)) of the
+    # 65k-token cache geometry, through compose_rebase_k_tokens
+    w = synth.WORKLOADS["long65k"]
+    geo = b.Geo.from_workload(w)
+    loc = synth.local_coords(w).astype(np.int64)
+    j = np.arange(w.n_tokens, dtype=np.int64)
+    toff_h = np.stack([j, j, j], axis=1) - loc
+    toff = torch.from_numpy(toff_h.astype(np.int32)).cuda()
+    moved = int(np.sum(np.any(toff_h != 0, axis=1)))
+    nbytes = 2 * w.n_layers * w.n_kv_heads * moved * w.head_dim * 2
+    K0 = torch.empty((w.n_layers, w.n_kv_heads, w.n_tokens, w.head_dim), dtype=torch.bfloat16, device="cuda")
+    for layer in range(w.n_layers):
+        K0[layer] = synth.torch_normal((w.n_kv_heads, w.n_tokens, w.head_dim), w.seed, 0, synth.TAG_K, layer,
+                                       "cuda", torch.bfloat16)
+    K = K0.clone()
+    for flush in (True, False):
+        def before(flush=flush):
+            K.copy_(K0)
+            if flush:
+                junk.fill_(7)
+        med, best = _events(torch, stream, lambda: b.compose_rebase_k_tokens(geo, K, toff), args.steps + 1, before)
+        gbps = nbytes / (med * 1e-3) / 1e9
+        rows.append({"workload": "long65k, per-token scalar offsets", "tokens": w.n_tokens, "bytes": nbytes,
+                     "flush": flush, "ms": round(med, 4), "ms_min": round(best, 4), "GBps": round(gbps, 1),
+                     "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
+        log(f"[bench] long65k scalar per-token flush={flush}: {med * 1e3:.1f} us, {gbps:.1f} GB/s")
+    del K0, K
     print(json.dumps({"metric": "rebase GB/s (% HBM peak) by cache size", "unit": "GB/s", "n_gpus": 1,
                       "higher_is_better": True, "dtype": "bf16", "data": "synthetic", "sweep": rows}), flush=True)
 

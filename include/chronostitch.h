@@ -108,6 +108,28 @@ cs_status compose_rebase_k(const cs_geometry* g, void* k_cache,
                            void* stream);
 
 /* ---------------------------------------------------------------------------
+ * compose_rebase_k_tokens -- Eq. 3 with one offset per token (the position
+ * policies compared in Section 3 and Table 1).
+ *
+ * Rotates every stored post-rotary key, in place, by its own token's offset:
+ * pair i of token t turns by Delta_t[sigma(i)] * theta_i, so f(x, p_t) becomes
+ * f(x, p_t + Delta_t).  With Delta_t equal to the chunk offset for every token
+ * of a chunk this is compose_rebase_k; a per-token offset expresses policies
+ * such as scalar re-basing, which moves token j of the composed cache to
+ * (j, j, j).  Angles are formed in float64 and reduced modulo 2*pi as in
+ * compose_rebase_k.  Tokens with Delta_t = (0,0,0) are not touched.
+ *
+ *   g              geometry (HOST)
+ *   k_cache        DEVICE [L][H_kv][T][D] keys, rotated in place
+ *   token_offsets  DEVICE int32 [T][3]: (dt, dh, dw) = p' - p of every token
+ *                  (read on the device; contents are not checked)
+ *   stream         hipStream_t or NULL
+ * Errors: CS_ERR_INVALID_ARGUMENT for a bad geometry or a NULL pointer,
+ * CS_ERR_HIP for a launch failure.                                          */
+cs_status compose_rebase_k_tokens(const cs_geometry* g, void* k_cache,
+                                  const int32_t* token_offsets, void* stream);
+
+/* ---------------------------------------------------------------------------
  * score_deviation_topk -- Section 2, Eq. 5 and the top-rho selection after it.
  *
  * For every later-chunk token t in [s_1, T):

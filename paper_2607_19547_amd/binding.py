@@ -49,6 +49,7 @@ def lib():
         vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         G = ctypes.POINTER(Geometry)
         L.compose_rebase_k.argtypes = [G, vp, vp, vp, vp, vp]
+        L.compose_rebase_k_tokens.argtypes = [G, vp, vp, vp]
         L.score_deviation_topk_workspace.argtypes = [G, ctypes.POINTER(sz)]
         L.score_deviation_topk.argtypes = [G, vp, i32, vp, ctypes.c_double, vp, vp,
                                            ctypes.POINTER(i64), vp, sz, vp]
@@ -60,7 +61,8 @@ def lib():
         L.cs_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(i64),
                                    ctypes.POINTER(ctypes.c_double)]
         L.cs_trace_count.restype = i32
-        for name in ("compose_rebase_k", "score_deviation_topk_workspace", "score_deviation_topk",
+        for name in ("compose_rebase_k", "compose_rebase_k_tokens", "score_deviation_topk_workspace",
+                     "score_deviation_topk",
                      "selective_attend_scatter_workspace", "selective_attend_scatter",
                      "cs_trace_enable", "cs_trace_collect", "cs_trace_get"):
             getattr(L, name).restype = ctypes.c_int
@@ -123,6 +125,11 @@ def compose_rebase_k(geo, k_cache, chunk_offsets, local_coords=None, want_global
                                   None if glob is None else glob.ctypes.data_as(ctypes.c_void_p),
                                   _stream(stream)))
     return glob
+
+
+def compose_rebase_k_tokens(geo, k_cache, token_offsets, stream=None):
+    """Re-base k_cache in place by a per-token offset (DEVICE int32 [T, 3] tensor)."""
+    _check(lib().compose_rebase_k_tokens(geo.ref, _ptr(k_cache), _ptr(token_offsets), _stream(stream)))
 
 
 def score_deviation_topk_workspace(geo):

@@ -155,6 +155,21 @@ cs_status compose_rebase_k(const cs_geometry* gp, void* k_cache, const int32_t* 
   return launch_rebase(g, k_cache, chunk_offsets, theta.data(), (hipStream_t)stream);
 }
 
+cs_status compose_rebase_k_tokens(const cs_geometry* gp, void* k_cache, const int32_t* token_offsets,
+                                  void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  if (!k_cache) return fail(CS_ERR_INVALID_ARGUMENT, "k_cache is NULL");
+  if (!token_offsets) return fail(CS_ERR_INVALID_ARGUMENT, "token_offsets is NULL");
+  std::vector<double> theta(g.P);
+  for (int i = 0; i < g.P; ++i)
+    theta[i] = gp->inv_freq ? gp->inv_freq[i] : pow(gp->rope_base, -2.0 * i / (double)g.D);
+  for (int i = 0; i < g.P; ++i)
+    if (!isfinite(theta[i])) return fail(CS_ERR_INVALID_ARGUMENT, "inv_freq holds a non-finite value");
+  return launch_rebase_tokens(g, k_cache, token_offsets, theta.data(), (hipStream_t)stream);
+}
+
 cs_status score_deviation_topk_workspace(const cs_geometry* gp, size_t* bytes) {
   Geo g;
   cs_status st = check_geometry(gp, &g);

@@ -68,6 +68,8 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float x) { return (uint16_t)(pac
 // ------------------------------------------------------------------ launches (per source file)
 cs_status launch_rebase(const Geo& g, void* k, const int32_t* offsets, const double* theta,
                         hipStream_t s);
+cs_status launch_rebase_tokens(const Geo& g, void* k, const int32_t* token_offsets, const double* theta,
+                               hipStream_t s);
 cs_status launch_score_select(const Geo& g, const void* k_layer, const void* k_fresh, float* scores,
                               int32_t* sel, int64_t k_sel, hipStream_t s);
 cs_status launch_scatter(const Geo& g, void* k, void* v, int lb, int le, const int32_t* sel,

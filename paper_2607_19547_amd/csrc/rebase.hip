@@ -185,6 +185,131 @@ __global__ __launch_bounds__(256) void rebase_generic(const RebaseGenArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- per-token offsets
+// The same rotation with an offset per token (Section 3 compares position
+// policies whose offset differs from token to token, e.g. scalar re-basing).
+// A workgroup takes a block of kTokTB tokens and kTokPG planes: it first builds
+// the block's cos/sin table in LDS (angles in float64, the same reduction as
+// above), then streams the block's rows of its planes.  Rows whose token has
+// offset (0, 0, 0) are not touched.
+constexpr int kTokTB = 64;  // tokens per workgroup
+constexpr int kTokPG = 8;   // planes per workgroup
+constexpr int kTokTabW = 65;  // table row stride (float2): one pad entry spreads the LDS banks
+
+struct RebaseTokArgs {
+  void* k;
+  const int32_t* off;  // DEVICE [T][3]
+  int64_t T;
+  int planes, D, P;
+  int sec0, sec01;
+  double theta[256];
+};
+
+__global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokArgs a) {
+  __shared__ float2 tab[kTokTB * kTokTabW];
+  __shared__ int moved[kTokTB];
+  const int64_t t0 = (int64_t)blockIdx.x * kTokTB;
+  const int ntok = (int)min((int64_t)kTokTB, a.T - t0);
+  for (int e = threadIdx.x; e < kTokTB * 64; e += 256) {
+    const int tok = e >> 6, i = e & 63;
+    float2 cs = make_float2(1.f, 0.f);
+    if (tok < ntok) {
+      const int32_t* o = a.off + (t0 + tok) * 3;
+      cs = cos_sin_of((double)o[axis_of(i, a.sec0, a.sec01)] * a.theta[i]);
+    }
+    tab[tok * kTokTabW + i] = cs;
+  }
+  if (threadIdx.x < kTokTB) {
+    const int tok = threadIdx.x;
+    int mv = 0;
+    if (tok < ntok) {
+      const int32_t* o = a.off + (t0 + tok) * 3;
+      mv = (o[0] | o[1] | o[2]) != 0;
+    }
+    moved[tok] = mv;
+  }
+  __syncthreads();
+  uint16_t* k = (uint16_t*)a.k;
+  const int j = threadIdx.x & 7;
+  const int r0 = threadIdx.x >> 3;  // 0..31
+#pragma unroll 1
+  for (int it = 0; it < (kTokPG * kTokTB) / 32; it += 4) {
+    u32x4 wa[4], wb[4];
+    uint16_t* row[4];
+    int tk[4];
+    bool ok[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = (it + u) * 32 + r0;
+      const int plane = blockIdx.y * kTokPG + idx / kTokTB;
+      tk[u] = idx % kTokTB;
+      ok[u] = plane < a.planes && tk[u] < ntok && moved[tk[u]];
+      row[u] = k + ((int64_t)plane * a.T + t0 + tk[u]) * 128;
+      if (ok[u]) {
+        wa[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 8 * j));
+        wb[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 64 + 8 * j));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (ok[u]) {
+        float cs_[8], sn_[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float2 t = tab[tk[u] * kTokTabW + 8 * j + e];
+          cs_[e] = t.x;
+          sn_[e] = t.y;
+        }
+        rotate8(wa[u], wb[u], cs_, sn_);
+        __builtin_nontemporal_store(wa[u], (u32x4*)(row[u] + 8 * j));
+        __builtin_nontemporal_store(wb[u], (u32x4*)(row[u] + 64 + 8 * j));
+      }
+    }
+  }
+}
+
+// Any head_dim and either dtype: one workgroup per (token, plane), one pair per thread.
+template <typename E>
+__global__ __launch_bounds__(64) void rebase_tokens_generic(const RebaseTokArgs a) {
+  const int64_t t = blockIdx.x;
+  const int plane = blockIdx.y;
+  const int32_t* o = a.off + t * 3;
+  if ((o[0] | o[1] | o[2]) == 0) return;  // whole workgroup
+  E* row = (E*)a.k + ((int64_t)plane * a.T + t) * a.D;
+  for (int i = threadIdx.x; i < a.P; i += blockDim.x) {
+    const float2 cs = cos_sin_of((double)o[axis_of(i, a.sec0, a.sec01)] * a.theta[i]);
+    const float x = ld(row + i), y = ld(row + i + a.P);
+    st(row + i, fmaf(x, cs.x, -y * cs.y));
+    st(row + i + a.P, fmaf(x, cs.y, y * cs.x));
+  }
+}
+
+cs_status launch_rebase_tokens(const Geo& g, void* k, const int32_t* off, const double* theta, hipStream_t s) {
+  RebaseTokArgs a;
+  a.k = k;
+  a.off = off;
+  a.T = g.T;
+  a.planes = g.L * g.Hkv;
+  a.D = g.D;
+  a.P = g.P;
+  a.sec0 = g.sec[0];
+  a.sec01 = g.sec[0] + g.sec[1];
+  for (int i = 0; i < g.P; ++i) a.theta[i] = theta[i];
+  if (g.dtype == CS_BF16 && g.D == 128) {
+    TraceScope tr("rebase_tokens_bf16_d128", s);
+    hipLaunchKernelGGL(rebase_tokens_bf16_d128, dim3((unsigned)((g.T + kTokTB - 1) / kTokTB),
+                                                     (unsigned)((a.planes + kTokPG - 1) / kTokPG)),
+                       dim3(256), 0, s, a);
+  } else {
+    TraceScope tr("rebase_tokens_generic", s);
+    if (g.dtype == CS_BF16)
+      hipLaunchKernelGGL(rebase_tokens_generic<uint16_t>, dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a);
+    else
+      hipLaunchKernelGGL(rebase_tokens_generic<float>, dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a);
+  }
+  return check_launch("per-token rebase kernel launch");
+}
+
 // ---------------------------------------------------------------- host launcher
 cs_status launch_rebase(const Geo& g, void* k, const int32_t* off, const double* theta,
                         hipStream_t s) {

@@ -74,6 +74,14 @@ def test_rebase_argument_errors(built_lib):
     assert _code(b.compose_rebase_k, bad_base, FAKE, np.zeros((2, 3)), stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
 
 
+def test_rebase_tokens_argument_errors(built_lib):
+    g = _geo()
+    assert _code(b.compose_rebase_k_tokens, g, None, FAKE, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    assert _code(b.compose_rebase_k_tokens, g, FAKE, None, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    code, text = _code(b.compose_rebase_k_tokens, _geo(sections=(2, 3, 4)), FAKE, FAKE, stream=0)
+    assert code == b.CS_ERR_INVALID_ARGUMENT and "sum" in text
+
+
 def test_host_coordinate_shift_without_device_work(built_lib):
     """global = local + offset of the token's chunk; a geometry with every
     offset zero enqueues no kernel, so this runs on a CPU-only host."""

@@ -470,3 +470,66 @@ def test_more_than_1024_row_tiles():
     w = ragged(n_layers=1, G=32, Hkv=1, chunk_lens=(64, 9000))
     log(f"case ragged G=32 Hkv=1 lens=(64, 9000) rho=1")
     _isolated_full_size(w, rhos=(1.0,), n_random=64, check_rebase=False)
+
+
+# ======================================================================== per-token rebase (Section 3 policies)
+def _gpu_rebase_tokens(w, k_stored, toff):
+    b = B()
+    geo = b.Geo.from_workload(w)
+    K = to_dev(k_stored, w.dtype)
+    O = torch.from_numpy(np.ascontiguousarray(toff, dtype=np.int32)).cuda()
+    b.compose_rebase_k_tokens(geo, K, O)
+    torch.cuda.synchronize()
+    return to_host(K, w.dtype)
+
+
+@pytest.mark.parametrize("name", ["qwen8k", "tiny", "bf16_d32"])
+def test_rebase_tokens_policies(name, request):
+    """Every policy's per-token offsets, GPU against the oracle's Eq. 3 per token;
+    the three-axis offsets give exactly the per-chunk kernel's bits; the layer-0
+    fidelity of the GPU's keys keeps Table 1's ordering."""
+    if name == "bf16_d32":   # the generic kernel in bf16
+        w = dataclasses.replace(synth.WORKLOADS["tiny"], name="bf16_d32", dtype="bf16", head_dim=32,
+                                sections=(4, 6, 6), n_layers=2, score_layer=1)
+    else:
+        w = synth.WORKLOADS[name]
+    log(f"case rebase_tokens {name}")
+    d = request.getfixturevalue("qwen8k")[1] if name == "qwen8k" else oracle.inputs.build(w)
+    th, sg = theta_sigma(w)
+    loc, cs, off = d["local_coords"], d["chunk_start"], d["chunk_offsets"]
+    out = {}
+    for p in oracle.policies.POLICIES:
+        toff = oracle.policies.token_offsets(p, loc, cs, off)
+        got = _gpu_rebase_tokens(w, d["k_stored"], toff)
+        want = oracle.rebase.rebase_tokens_stored(d["k_stored"], w.dtype, toff, th, sg)
+        g, o = dec(got, w.dtype), dec(want, w.dtype)
+        tol = ulp(o, w.dtype) + 2.0 ** -20 * pair_norm(o)
+        assert np.all(np.abs(g - o) <= tol), p
+        still = ~np.any(toff != 0, axis=1)
+        assert np.array_equal(got[:, :, still], d["k_stored"][:, :, still])
+        out[p] = got
+    b = B()
+    K = to_dev(d["k_stored"], w.dtype)
+    b.compose_rebase_k(b.Geo.from_workload(w), K, off)
+    assert np.array_equal(to_host(K, w.dtype), out["three_axis"])
+    if w.n_tokens >= 1024:
+        # layer 0 of Table 1 on the GPU's keys: joint keys from the oracle's own Eq. 2
+        joint = oracle.rebase.rebase_tokens_f64(dec(d["k_stored"][0], w.dtype),
+                                                oracle.policies.token_offsets("three_axis", loc, cs, off), th, sg)
+        fid = {p: oracle.policies.fidelity(dec(out[p][0], w.dtype), joint) for p in out}
+        log(f"  layer-0 fidelity {name}: " + ", ".join(f"{p} cos {c:.4f} relMSE {r:.2e}" for p, (c, r) in fid.items()))
+        assert fid["three_axis"][1] < 1e-4 and fid["naive"][1] > 1e-2 and fid["scalar1d"][1] > fid["naive"][1]
+
+
+def test_rebase_tokens_long65k_scalar1d():
+    """Scalar re-basing of the timed cache geometry (65,536 tokens; every token
+    moves on all three axes), first two layers, every element against the oracle."""
+    w = dataclasses.replace(synth.WORKLOADS["long65k"], n_layers=2)
+    log("case rebase_tokens long65k scalar1d")
+    d = oracle.inputs.build(w, q_layers=[0])
+    th, sg = theta_sigma(w)
+    toff = oracle.policies.token_offsets("scalar1d", d["local_coords"], d["chunk_start"], d["chunk_offsets"])
+    got = _gpu_rebase_tokens(w, d["k_stored"], toff)
+    want = oracle.rebase.rebase_tokens_stored(d["k_stored"], w.dtype, toff, th, sg)
+    g, o = dec(got, w.dtype), dec(want, w.dtype)
+    assert np.all(np.abs(g - o) <= ulp(o, w.dtype) + 2.0 ** -20 * pair_norm(o))
