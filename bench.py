@@ -50,6 +50,9 @@ def parse():
     p.add_argument("--cpu-baseline", type=int, default=1, help="time the CPU oracle on a sample (0: skip)")
     p.add_argument("--batched-layers", type=int, default=0,
                    help="one selective_attend_scatter call over all layers instead of one per layer")
+    p.add_argument("--fused-rope-steps", type=int, default=3,
+                   help="steps also timed through selective_attend_scatter_rope (pre-rotary fresh rows, "
+                        "rotated at the global coordinates; 0: skip)")
     p.add_argument("--batched-steps", type=int, default=3,
                    help="steps also timed with one batched attention call over all layers (0: skip)")
     p.add_argument("--sweep", choices=("none", "rebase", "attention"), default="none",
@@ -86,6 +89,12 @@ class Inputs:
             self.KF[layer] = (kreb[layer, :, cs1:].float() + s * zk).to(bf)
             self.VF[layer] = (self.V0[layer, :, cs1:].float() + s * zv).to(bf)
         del kreb
+        loc = synth.local_coords(w).astype(np.int64)
+        glob = loc.copy()
+        cs = w.chunk_start
+        for c in range(w.n_chunks):
+            glob[cs[c]:cs[c + 1]] += self.offsets[c]
+        self.coords = torch.from_numpy(glob.astype(np.int32)).to(dev)   # global coordinates [T, 3]
         self.K = self.K0.clone()
         self.V = self.V0.clone()
         torch.cuda.synchronize()
@@ -98,11 +107,15 @@ def busy_gpu(torch):
     torch.cuda._sleep(400_000)
 
 
-def run_compose(inp, w, rho, binding, torch, out, lse, sel, scores, ws, batched):
+def run_compose(inp, w, rho, binding, torch, out, lse, sel, scores, ws, batched, fused=False):
     b = binding
     b.compose_rebase_k(inp.geo, inp.K, inp.offsets)
     k = b.score_deviation_topk(inp.geo, inp.K, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
-    if batched:
+    if fused:   # QF and KF taken as the pre-rotary fresh rows (N(0, 1) either way)
+        for layer in range(w.n_layers):
+            b.selective_attend_scatter_rope(inp.geo, inp.K, inp.V, layer, layer + 1, sel, k, inp.QF, inp.KF,
+                                            inp.VF, inp.coords, out, lse, ws)
+    elif batched:
         b.selective_attend_scatter(inp.geo, inp.K, inp.V, 0, w.n_layers, sel, k, inp.QF, inp.KF, inp.VF,
                                    out, lse, ws)
     else:
@@ -139,11 +152,14 @@ def main():
     other = None
     if args.batched_steps > 0:  # the other launch mode, for comparison
         other = bench_rho(inp, w, rho, args.batched_steps, 1, binding, torch, not args.batched_layers)
+    fused = None
+    if args.fused_rope_steps > 0:
+        fused = bench_rho(inp, w, rho, args.fused_rope_steps, 1, binding, torch, False, fused=True)
     cpu = cpu_baseline(w, rho) if args.cpu_baseline else None
-    emit(args, w, rho, result, rho1, cpu, other)
+    emit(args, w, rho, result, rho1, cpu, other, fused)
 
 
-def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched):
+def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False):
     b = binding
     n = w.n_candidates
     scores = torch.empty(n, dtype=torch.float32, device="cuda")
@@ -152,7 +168,8 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched):
     k = b.score_deviation_topk(inp.geo, inp.K, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
     out = torch.empty((w.n_layers, w.n_q_heads, k, w.head_dim), dtype=torch.bfloat16, device="cuda")
     lse = torch.empty((w.n_layers, w.n_q_heads, k), dtype=torch.float32, device="cuda")
-    ws_bytes = b.selective_attend_scatter_workspace(inp.geo, k, w.n_layers if batched else 1)
+    ws_bytes = (b.selective_attend_scatter_rope_workspace(inp.geo, k, 1) if fused else
+                b.selective_attend_scatter_workspace(inp.geo, k, w.n_layers if batched else 1))
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
     log(f"[bench] rho={rho}: n_sel={k}, workspace {ws_bytes / 2**20:.1f} MiB, warmup {warmup}, steps {steps}")
@@ -163,7 +180,7 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched):
 
     for _ in range(warmup):
         restore()
-        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched)
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused)
     torch.cuda.synchronize()
     b.cs_trace_reset()
     times = []
@@ -176,7 +193,7 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched):
         busy_gpu(torch)
         b.cs_trace_enable(True)
         e0.record(stream)
-        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched)
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused)
         e1.record(stream)
         b.cs_trace_enable(False)
         torch.cuda.synchronize()
@@ -382,7 +399,7 @@ def _traffic(kernel):
         return None
 
 
-def emit(args, w, rho, r, rho1, cpu, other=None):
+def emit(args, w, rho, r, rho1, cpu, other=None, fused=None):
     tr = r["trace"]
     steps = r["steps"]
     attn_n, attn_ms = tr.get("sel_attn_mfma", (0, 0.0))
@@ -442,6 +459,11 @@ def emit(args, w, rho, r, rho1, cpu, other=None):
     }
     if other is not None:
         line["per_layer_compose_ms" if args.batched_layers else "batched_compose_ms"] = round(other["ms"], 4)
+    if fused is not None:
+        line["fused_rope_compose_ms"] = round(fused["ms"], 4)
+        fr = fused["trace"].get("rope_scatter_bf16_d128")
+        if fr:
+            line["fused_rope_scatter_us_per_layer"] = round(fr[1] / fr[0] * 1e3, 2)
     if rho1 is not None:
         line["rho1_compose_ms"] = round(rho1["ms"], 3)
         line["rho1_over_rho_speedup"] = round(rho1["ms"] / r["ms"], 3)

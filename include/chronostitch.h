@@ -164,6 +164,47 @@ cs_status score_deviation_topk(const cs_geometry* g, const void* k_cache,
                                size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * selective_attend_scatter_rope -- selective_attend_scatter with the rotary
+ * embedding of the recomputed rows fused in (Eq. 2 at the global coordinates
+ * p' of Section 2).
+ *
+ * The recompute of a selected token applies RoPE at its global coordinate;
+ * here the caller hands over the PRE-rotary fresh queries and keys and the
+ * global coordinates, and only the selected rows are rotated: for each layer,
+ *   1. K row of selected token t (every KV head): f(k_pre, p'_t), rounded to
+ *      the storage dtype, scattered into the cache; V rows are scattered as in
+ *      selective_attend_scatter;
+ *   2. Q row (every query head): f(q_pre, p'_t), rounded to the storage
+ *      dtype, kept in the workspace;
+ *   3. attention exactly as in selective_attend_scatter.
+ * The result equals selective_attend_scatter on q_fresh = f(q_pre, p') and
+ * k_fresh = f(k_pre, p') rounded the same way.  Angles are formed in float64
+ * and reduced modulo 2*pi (float32 cos/sin), as in compose_rebase_k.
+ *
+ *   q_pre          DEVICE [L][H_q][n][D] pre-rotary fresh queries
+ *   k_pre          DEVICE [L][H_kv][n][D] pre-rotary fresh keys
+ *   v_fresh        DEVICE [L][H_kv][n][D] fresh values
+ *   coords         DEVICE int32 [T][3] global coordinates p' of every token
+ *                  (compose_rebase_k's global_coords, copied to the device)
+ *   workspace      DEVICE, >= selective_attend_scatter_rope_workspace() for
+ *                  the same n_sel and n_layers_per_call >= layer_end -
+ *                  layer_begin: the attention's partials plus the rotated
+ *                  queries (n_layers x H_q x n_sel x D elements)
+ *   other arguments as for selective_attend_scatter.
+ * Errors: CS_ERR_INVALID_ARGUMENT, CS_ERR_WORKSPACE_TOO_SMALL, CS_ERR_HIP. */
+cs_status selective_attend_scatter_rope_workspace(const cs_geometry* g, int64_t n_sel,
+                                                  int32_t n_layers_per_call,
+                                                  size_t* bytes);
+cs_status selective_attend_scatter_rope(const cs_geometry* g, void* k_cache,
+                                        void* v_cache, int32_t layer_begin,
+                                        int32_t layer_end, const int32_t* sel_idx,
+                                        int64_t n_sel, const void* q_pre,
+                                        const void* k_pre, const void* v_fresh,
+                                        const int32_t* coords, void* out,
+                                        float* lse, void* workspace,
+                                        size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * selective_attend_scatter -- Section 2, Eq. 1 and the repair step.
  *
  * For each layer l in [layer_begin, layer_end):

@@ -54,6 +54,9 @@ def lib():
         L.score_deviation_topk.argtypes = [G, vp, i32, vp, ctypes.c_double, vp, vp,
                                            ctypes.POINTER(i64), vp, sz, vp]
         L.selective_attend_scatter_workspace.argtypes = [G, i64, i32, ctypes.POINTER(sz)]
+        L.selective_attend_scatter_rope_workspace.argtypes = [G, i64, i32, ctypes.POINTER(sz)]
+        L.selective_attend_scatter_rope.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp, vp,
+                                                    vp, sz, vp]
         L.selective_attend_scatter.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp,
                                                vp, sz, vp]
         L.cs_last_error.restype = ctypes.c_char_p
@@ -64,6 +67,7 @@ def lib():
         for name in ("compose_rebase_k", "compose_rebase_k_tokens", "score_deviation_topk_workspace",
                      "score_deviation_topk",
                      "selective_attend_scatter_workspace", "selective_attend_scatter",
+                     "selective_attend_scatter_rope_workspace", "selective_attend_scatter_rope",
                      "cs_trace_enable", "cs_trace_collect", "cs_trace_get"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -186,3 +190,20 @@ def cs_trace_collect():
         _check(L.cs_trace_get(i, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms)))
         out[name.value.decode()] = (n.value, ms.value)
     return out
+
+
+def selective_attend_scatter_rope_workspace(geo, n_sel, n_layers_per_call):
+    n = ctypes.c_size_t(0)
+    _check(lib().selective_attend_scatter_rope_workspace(geo.ref, int(n_sel), int(n_layers_per_call),
+                                                         ctypes.byref(n)))
+    return n.value
+
+
+def selective_attend_scatter_rope(geo, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre,
+                                  v_fresh, coords, out, lse=None, workspace=None, stream=None):
+    """selective_attend_scatter on pre-rotary fresh Q/K, rotated at the global coordinates (DEVICE int32 [T, 3])."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().selective_attend_scatter_rope(geo.ref, _ptr(k_cache), _ptr(v_cache), int(layer_begin),
+                                               int(layer_end), _ptr(sel_idx), int(n_sel), _ptr(q_pre), _ptr(k_pre),
+                                               _ptr(v_fresh), _ptr(coords), _ptr(out), _ptr(lse), _ptr(workspace),
+                                               ws_bytes, _stream(stream)))

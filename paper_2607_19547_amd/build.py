@@ -14,7 +14,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB_DIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIB_DIR, "libchronostitch.so")
-SOURCES = ["api.hip", "rebase.hip", "score_select.hip", "attention.hip"]
+SOURCES = ["api.hip", "rebase.hip", "score_select.hip", "attention.hip", "rope_scatter.hip"]
 # attention.hip never produces or consumes NaN (masked scores are -inf and the
 # running max is guarded), so max reductions need no NaN canonicalisation
 EXTRA = {"attention.hip": ["-fno-honor-nans"]}

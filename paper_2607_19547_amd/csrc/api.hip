@@ -246,8 +246,66 @@ cs_status selective_attend_scatter(const cs_geometry* gp, void* k_cache, void* v
   hipStream_t s = (hipStream_t)stream;
   st = launch_scatter(g, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, k_fresh, v_fresh, s);
   if (st) return st;
-  return launch_attention(g, p, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_fresh,
+  return launch_attention(g, p, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_fresh, false,
                           out, lse, workspace, s);
+}
+
+// Workspace of the fused-rotary variant: the attention's, then the rotated
+// queries [layers in call][H_q][n_sel][D].
+static size_t rope_ws(const Geo& g, const AttnPlan& p, int64_t n_sel, int layers, size_t* att_bytes) {
+  const size_t att = p.mfma && n_sel > 0 && layers > 0 ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)layers : 0;
+  *att_bytes = align_up(att, 256);
+  return *att_bytes + (size_t)layers * g.Hq * n_sel * g.D * g.esize;
+}
+
+cs_status selective_attend_scatter_rope_workspace(const cs_geometry* gp, int64_t n_sel, int32_t n_layers_per_call,
+                                                  size_t* bytes) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  if (!bytes) return fail(CS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  if (n_sel < 0 || n_sel > g.n) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel must be in [0, n]");
+  if (n_layers_per_call < 0 || n_layers_per_call > g.L)
+    return fail(CS_ERR_INVALID_ARGUMENT, "n_layers_per_call must be in [0, n_layers]");
+  AttnPlan p = plan_attention(g, n_sel, n_layers_per_call);
+  size_t att = 0;
+  *bytes = n_sel > 0 && n_layers_per_call > 0 ? rope_ws(g, p, n_sel, n_layers_per_call, &att) : 0;
+  return CS_OK;
+}
+
+cs_status selective_attend_scatter_rope(const cs_geometry* gp, void* k_cache, void* v_cache, int32_t layer_begin,
+                                        int32_t layer_end, const int32_t* sel_idx, int64_t n_sel,
+                                        const void* q_pre, const void* k_pre, const void* v_fresh,
+                                        const int32_t* coords, void* out, float* lse, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  if (layer_begin < 0 || layer_end < layer_begin || layer_end > g.L)
+    return fail(CS_ERR_INVALID_ARGUMENT, "need 0 <= layer_begin <= layer_end <= n_layers");
+  if (n_sel < 0 || n_sel > g.n) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel must be in [0, n]");
+  if (n_sel == 0 || layer_end == layer_begin) return CS_OK;
+  if (!k_cache || !v_cache || !sel_idx || !q_pre || !k_pre || !v_fresh || !coords || !out)
+    return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  std::vector<double> theta(g.P);
+  for (int i = 0; i < g.P; ++i)
+    theta[i] = gp->inv_freq ? gp->inv_freq[i] : pow(gp->rope_base, -2.0 * i / (double)g.D);
+  for (int i = 0; i < g.P; ++i)
+    if (!isfinite(theta[i])) return fail(CS_ERR_INVALID_ARGUMENT, "inv_freq holds a non-finite value");
+  const int layers = layer_end - layer_begin;
+  AttnPlan p = plan_attention(g, n_sel, layers);
+  size_t att = 0;
+  const size_t need = rope_ws(g, p, n_sel, layers, &att);
+  if (!workspace || workspace_bytes < need)
+    return fail(CS_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than selective_attend_scatter_rope_workspace() (" +
+                                                std::to_string(need) + " bytes)");
+  hipStream_t s = (hipStream_t)stream;
+  void* q_ws = (char*)workspace + att;
+  st = launch_rope_scatter(g, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords,
+                           theta.data(), q_ws, s);
+  if (st) return st;
+  return launch_attention(g, p, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_ws, true, out, lse,
+                          workspace, s);
 }
 
 // ------------------------------------------------------------------ tracing exports

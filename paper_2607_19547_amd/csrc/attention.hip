@@ -123,6 +123,7 @@ struct AttnArgs {
   int64_t T, n, n_sel, n_tiles;
   int cs1, Hq, Hkv, lb, layers;
   int part_cap;      // partial slots per layer
+  int q_by_slot;     // q is [layers in call][H_q][n_sel][128] (rows in selection order), else [L][H_q][n][128]
   float scale_log2;  // log2(e) / sqrt(D)
 };
 
@@ -501,7 +502,9 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
 
   bf16x8 qb[8];
   if (valid) {
-    const uint16_t* qp = a.q + (((int64_t)layer * a.Hq + h) * a.n + (g_q - a.cs1)) * 128 + 8 * hi;
+    const int64_t qrow = a.q_by_slot ? ((int64_t)lrel * a.Hq + h) * a.n_sel + m
+                                     : ((int64_t)layer * a.Hq + h) * a.n + (g_q - a.cs1);
+    const uint16_t* qp = a.q + qrow * 128 + 8 * hi;
 #pragma unroll
     for (int s = 0; s < 8; ++s) qb[s] = *(const bf16x8*)(qp + 16 * s);
   } else {
@@ -759,6 +762,7 @@ struct GenAttnArgs {
   float* lse;
   int64_t T, n, n_sel;
   int cs1, Hq, Hkv, G, D, lb;
+  int q_by_slot;
   float scale;
 };
 
@@ -797,7 +801,8 @@ __global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a) {
   const int t = a.sel[m];
   if (t < a.cs1 || t >= a.T) return;  // out-of-contract index
   const int kv = h / a.G;
-  const E* qp = (const E*)a.q + (((int64_t)layer * a.Hq + h) * a.n + (t - a.cs1)) * a.D;
+  const E* qp = (const E*)a.q + (a.q_by_slot ? ((int64_t)blockIdx.z * a.Hq + h) * a.n_sel + m
+                                             : ((int64_t)layer * a.Hq + h) * a.n + (t - a.cs1)) * a.D;
   const E* kb = (const E*)a.k + ((int64_t)layer * a.Hkv + kv) * a.T * a.D;
   const E* vb = (const E*)a.v + ((int64_t)layer * a.Hkv + kv) * a.T * a.D;
   for (int d = lane; d < a.D; d += 64) qs[d] = gld(qp + d);
@@ -906,8 +911,8 @@ static void launch_mfma_g(const AttnArgs& a, hipStream_t s) {
 }
 
 cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const void* v, int lb, int le,
-                           const int32_t* sel, int64_t n_sel, const void* qf, void* out, float* lse, void* ws,
-                           hipStream_t s) {
+                           const int32_t* sel, int64_t n_sel, const void* qf, bool q_by_slot, void* out, float* lse,
+                           void* ws, hipStream_t s) {
   const int layers = le - lb;
   if (p.mfma) {
     AttnArgs a;
@@ -930,6 +935,7 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const
     a.lb = lb;
     a.layers = layers;
     a.part_cap = p.part_cap;
+    a.q_by_slot = q_by_slot ? 1 : 0;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g.D));
     switch (g.G) {
       case 1: launch_mfma_g<1>(a, s); break;
@@ -944,6 +950,7 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const
   }
   GenAttnArgs a;
   a.q = qf;
+  a.q_by_slot = q_by_slot ? 1 : 0;
   a.k = k;
   a.v = v;
   a.sel = sel;

@@ -65,6 +65,48 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 __device__ __forceinline__ uint16_t f32_to_bf16(float x) { return (uint16_t)(pack_bf16x2(x, 0.f) & 0xffffu); }
 
+// ------------------------------------------------------------------ rotation (Eq. 2, Eq. 3)
+// cos/sin of a rotary angle formed in float64: reduced modulo 2*pi, evaluated
+// in float64 and rounded once to float32.
+// 2*pi = C1 + C2 + C3 with C1, C2 holding 26 significant bits each, so
+// k*C1 and k*C2 are exact for |k| < 2^27.
+#define CS_TWO_PI_C1 0x1.921fb50000000p+2
+#define CS_TWO_PI_C2 0x1.110b460000000p-24
+#define CS_TWO_PI_C3 0x1.1a62633145c07p-52
+#define CS_INV_TWO_PI 0x1.45f306dc9c883p-3
+
+__device__ __forceinline__ float2 cos_sin_of(double phi) {
+  double k = rint(phi * CS_INV_TWO_PI);
+  double r = phi;
+  if (fabs(k) < 134217728.0) {  // 2^27
+    r = fma(-k, CS_TWO_PI_C1, r);
+    r = fma(-k, CS_TWO_PI_C2, r);
+    r = fma(-k, CS_TWO_PI_C3, r);
+  }
+  double s, c;
+  sincos(r, &s, &c);
+  return make_float2((float)c, (float)s);
+}
+
+__device__ __forceinline__ int axis_of(int i, int sec0, int sec01) {
+  return i < sec0 ? 0 : (i < sec01 ? 1 : 2);
+}
+
+// Rotates 8 rotary pairs held as bf16: wa = elements 8j..8j+7 of the first
+// half-row, wb = the same of the second half (pair i = (i, i + 64)).
+__device__ __forceinline__ void rotate8(u32x4& wa, u32x4& wb, const float* c, const float* s) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    float a0 = bf16_lo(wa[w]), a1 = bf16_hi(wa[w]);
+    float b0 = bf16_lo(wb[w]), b1 = bf16_hi(wb[w]);
+    float c0 = c[2 * w], s0 = s[2 * w], c1 = c[2 * w + 1], s1 = s[2 * w + 1];
+    float na0 = fmaf(a0, c0, -b0 * s0), nb0 = fmaf(a0, s0, b0 * c0);
+    float na1 = fmaf(a1, c1, -b1 * s1), nb1 = fmaf(a1, s1, b1 * c1);
+    wa[w] = pack_bf16x2(na0, na1);
+    wb[w] = pack_bf16x2(nb0, nb1);
+  }
+}
+
 // ------------------------------------------------------------------ launches (per source file)
 cs_status launch_rebase(const Geo& g, void* k, const int32_t* offsets, const double* theta,
                         hipStream_t s);
@@ -86,6 +128,9 @@ struct AttnPlan {
 AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call);
 cs_status launch_attention(const Geo& g, const AttnPlan& plan, const void* k, const void* v,
                            int lb, int le, const int32_t* sel, int64_t n_sel, const void* qf,
-                           void* out, float* lse, void* ws, hipStream_t s);
+                           bool q_by_slot, void* out, float* lse, void* ws, hipStream_t s);
+cs_status launch_rope_scatter(const Geo& g, void* k, void* v, int lb, int le, const int32_t* sel, int64_t n_sel,
+                              const void* q_pre, const void* k_pre, const void* v_new, const int32_t* coords,
+                              const double* theta, void* q_ws, hipStream_t s);
 
 }  // namespace cs

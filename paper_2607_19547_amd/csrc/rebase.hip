@@ -16,30 +16,6 @@
 
 namespace cs {
 
-// 2*pi = C1 + C2 + C3 with C1, C2 holding 26 significant bits each, so
-// k*C1 and k*C2 are exact for |k| < 2^27.
-#define CS_TWO_PI_C1 0x1.921fb50000000p+2
-#define CS_TWO_PI_C2 0x1.110b460000000p-24
-#define CS_TWO_PI_C3 0x1.1a62633145c07p-52
-#define CS_INV_TWO_PI 0x1.45f306dc9c883p-3
-
-__device__ __forceinline__ float2 cos_sin_of(double phi) {
-  double k = rint(phi * CS_INV_TWO_PI);
-  double r = phi;
-  if (fabs(k) < 134217728.0) {  // 2^27
-    r = fma(-k, CS_TWO_PI_C1, r);
-    r = fma(-k, CS_TWO_PI_C2, r);
-    r = fma(-k, CS_TWO_PI_C3, r);
-  }
-  double s, c;
-  sincos(r, &s, &c);
-  return make_float2((float)c, (float)s);
-}
-
-__device__ __forceinline__ int axis_of(int i, int sec0, int sec01) {
-  return i < sec0 ? 0 : (i < sec01 ? 1 : 2);
-}
-
 // ---------------------------------------------------------------- bf16, D = 128
 constexpr int kFastMaxChunks = 128;
 constexpr int kFastTB = 64;  // tokens per workgroup
@@ -60,18 +36,6 @@ struct RebaseFastArgs {
   int off[kFastMaxChunks][3];
 };
 
-__device__ __forceinline__ void rotate8(u32x4& wa, u32x4& wb, const float* c, const float* s) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    float a0 = bf16_lo(wa[w]), a1 = bf16_hi(wa[w]);
-    float b0 = bf16_lo(wb[w]), b1 = bf16_hi(wb[w]);
-    float c0 = c[2 * w], s0 = s[2 * w], c1 = c[2 * w + 1], s1 = s[2 * w + 1];
-    float na0 = fmaf(a0, c0, -b0 * s0), nb0 = fmaf(a0, s0, b0 * c0);
-    float na1 = fmaf(a1, c1, -b1 * s1), nb1 = fmaf(a1, s1, b1 * c1);
-    wa[w] = pack_bf16x2(na0, na1);
-    wb[w] = pack_bf16x2(nb0, nb1);
-  }
-}
 
 // Lane layout: 8 lanes per 256-byte row; lane j of the row owns pairs
 // 8j..8j+7, i.e. 16 bytes in each half of the row.  A workgroup of 256

@@ -142,3 +142,22 @@ def test_attention_workspace_sizing(built_lib):
         assert code == b.CS_ERR_WORKSPACE_TOO_SMALL
     # the fp32 path needs no workspace
     assert b.selective_attend_scatter_workspace(_geo(), 8, 1) == 0
+
+
+def test_fused_rope_argument_errors_and_workspace(built_lib):
+    g = _geo()
+    args = (g, FAKE, FAKE, 0, 1, FAKE, 4, FAKE, FAKE, FAKE, None, FAKE)
+    assert _code(b.selective_attend_scatter_rope, *args, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT  # NULL coords
+    assert _code(b.selective_attend_scatter_rope, g, FAKE, FAKE, 0, 1, FAKE, 33, FAKE, FAKE, FAKE, FAKE, FAKE,
+                 stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT                                          # n_sel > n
+    # the fp32 path still needs room for the rotated queries: n_layers x H_q x n_sel x D x 4 bytes
+    assert b.selective_attend_scatter_rope_workspace(g, 8, 1) == 1 * 4 * 8 * 16 * 4
+    small = type("W", (), {"data_ptr": lambda self: 0x1000, "numel": lambda self: 16,
+                           "element_size": lambda self: 1})()
+    code, _ = _code(b.selective_attend_scatter_rope, g, FAKE, FAKE, 0, 1, FAKE, 8, FAKE, FAKE, FAKE, FAKE, FAKE,
+                    workspace=small, stream=0)
+    assert code == b.CS_ERR_WORKSPACE_TOO_SMALL
+    q = b.Geo(36, 16, 2, 128, (16, 24, 24), "bf16", np.arange(33) * 2048)
+    assert (b.selective_attend_scatter_rope_workspace(q, 6349, 1)
+            >= b.selective_attend_scatter_workspace(q, 6349, 1) + 16 * 6349 * 128 * 2)
+    b.selective_attend_scatter_rope(g, None, None, 0, 1, None, 0, None, None, None, None, None, stream=0)  # nothing to do

@@ -533,3 +533,68 @@ def test_rebase_tokens_long65k_scalar1d():
     want = oracle.rebase.rebase_tokens_stored(d["k_stored"], w.dtype, toff, th, sg)
     g, o = dec(got, w.dtype), dec(want, w.dtype)
     assert np.all(np.abs(g - o) <= ulp(o, w.dtype) + 2.0 ** -20 * pair_norm(o))
+
+
+# ======================================================================== fused rotary embedding of fresh rows (f2)
+def _prerotary_fresh(w, d, layers):
+    """Pre-rotary fresh queries and keys in the storage dtype (the generator's draws; the fresh key is
+    the stored key's pre-rotary vector plus the token's noise, as in the oracle's input recipe)."""
+    s = synth.draw_token_scale(w)[None, :, None]
+    enc = (lambda x: obf.encode(x)) if w.dtype == "bf16" else (lambda x: x.astype(np.float32))
+    qs, ks = [], []
+    for layer in layers:
+        t = synth.draw_layer(w, layer, ("k_pre", "zk", "q_pre"))
+        qs.append(enc(t["q_pre"]))
+        ks.append(enc(t["k_pre"][:, w.cs1:, :] + s * t["zk"]))
+    return np.stack(qs), np.stack(ks)
+
+
+@pytest.mark.parametrize("G,Hkv,lens,rho,dtype", [
+    (8, 2, (300, 400, 333), 0.2, "bf16"),
+    (2, 8, (100, 300, 200), 0.3, "bf16"),
+    (8, 2, (1000, 1500, 1700, 800), 0.05, "bf16"),    # cut row tiles
+    (2, 2, (32, 32), 0.25, "f32"),                    # generic kernels
+])
+def test_fused_rope_equals_prerotated(G, Hkv, lens, rho, dtype):
+    """GPU fused path against the oracle's own rotation of the same pre-rotary rows
+    followed by the oracle's scatter and attention."""
+    w = ragged(G=G, Hkv=Hkv, chunk_lens=lens)
+    if dtype == "f32":
+        w = dataclasses.replace(w, dtype="f32", head_dim=16, sections=(2, 3, 3))
+    log(f"case fused rope G={G} Hkv={Hkv} lens={lens} rho={rho} {dtype}")
+    d = oracle.inputs.build(w)
+    th, sg = theta_sigma(w)
+    glob = d["global_coords"]
+    k_reb = oracle.rebase.rebase_stored(d["k_stored"], w.dtype, d["chunk_start"], d["chunk_offsets"], th, sg)
+    sc = oracle.score.deviation_f32(dec(k_reb[w.score_layer], w.dtype), dec(d["k_fresh"][w.score_layer], w.dtype),
+                                    w.cs1)
+    sel = oracle.select.select_top(sc, oracle.select.n_select(rho, w.n_candidates), w.cs1)
+    q_pre, k_pre = _prerotary_fresh(w, d, range(w.n_layers))
+    enc = (lambda x: obf.encode(x)) if w.dtype == "bf16" else (lambda x: x.astype(np.float32))
+    q_rot = enc(oracle.rope.apply_mrope(dec(q_pre, w.dtype), glob[w.cs1:], th, sg))
+    k_rot = enc(oracle.rope.apply_mrope(dec(k_pre, w.dtype), glob[w.cs1:], th, sg))
+    b = B()
+    geo = b.Geo.from_workload(w)
+    K, V = to_dev(k_reb, w.dtype), to_dev(d["v_stored"], w.dtype)
+    Q, KP, VF = to_dev(q_pre, w.dtype), to_dev(k_pre, w.dtype), to_dev(d["v_fresh"], w.dtype)
+    C = torch.from_numpy(np.ascontiguousarray(glob, dtype=np.int32)).cuda()
+    S = torch.from_numpy(sel.astype(np.int32)).cuda()
+    k = len(sel)
+    out = empty((w.n_layers, w.n_q_heads, k, w.head_dim), w.dtype)
+    lse = torch.empty((w.n_layers, w.n_q_heads, k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(b.selective_attend_scatter_rope_workspace(geo, k, 1), 1), dtype=torch.uint8, device="cuda")
+    for layer in range(w.n_layers):
+        b.selective_attend_scatter_rope(geo, K, V, layer, layer + 1, S, k, Q, KP, VF, C, out, lse, ws)
+    torch.cuda.synchronize()
+    kp, vp, o, ls = to_host(K, w.dtype), to_host(V, w.dtype), to_host(out, w.dtype), lse.cpu().numpy()
+    for layer in range(w.n_layers):
+        kpo = oracle.attention.scatter_rows(k_reb[layer], k_rot[layer], sel, w.cs1)
+        vpo = oracle.attention.scatter_rows(d["v_stored"][layer], d["v_fresh"][layer], sel, w.cs1)
+        assert np.array_equal(vp[layer], vpo)
+        g_, o_ = dec(kp[layer], w.dtype), dec(kpo, w.dtype)
+        assert np.all(np.abs(g_ - o_) <= ulp(o_, w.dtype) + 2.0 ** -20 * pair_norm(o_))
+        other = np.ones(w.n_tokens, bool)
+        other[sel] = False
+        assert np.array_equal(kp[layer][:, other], k_reb[layer][:, other])
+        o_ref, lse_ref = oracle.attention.attend_rows(dec(q_rot[layer], w.dtype), o_, dec(vpo, w.dtype), sel, w.cs1)
+        check_attention(w, o[layer], ls[layer], o_ref, lse_ref, f"fused rope layer {layer}")
