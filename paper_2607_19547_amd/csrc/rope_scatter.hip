@@ -19,7 +19,7 @@
 
 namespace cs {
 
-constexpr int kRsTok = 32;      // selected tokens per workgroup
+constexpr int kRsTok = 8;       // selected tokens per workgroup
 constexpr int kRsTabW = 65;     // table row stride (float2): one pad entry spreads the LDS banks
 
 struct RopeScatterArgs {
@@ -64,47 +64,53 @@ __global__ __launch_bounds__(256) void rope_scatter_bf16_d128(const RopeScatterA
   const int r0 = threadIdx.x >> 3;  // 0..31
   const int rows_per_tok = 2 * a.Hkv + a.Hq;
   const int total = kRsTok * rows_per_tok;
+  // rows in batches of four per lane group: all loads of a batch before its stores
 #pragma unroll 1
-  for (int base = 0; base < total; base += 32) {
-    const int idx = base + r0;
-    if (idx >= total) break;
-    const int r = idx % kRsTok, kind = idx / kRsTok;  // kind: [0, Hkv) K, [Hkv, 2 Hkv) V, then Q heads
-    const int t = tok_of[r];
-    if (t < 0) continue;
-    const int64_t src_row = t - a.cs1;
-    if (kind < 2 * a.Hkv) {
-      const bool is_k = kind < a.Hkv;
-      const int h = is_k ? kind : kind - a.Hkv;
-      const uint16_t* src = (is_k ? a.k_pre : a.v_new) + (((int64_t)layer * a.Hkv + h) * a.n + src_row) * 128;
-      uint16_t* dst = (is_k ? a.k : a.v) + (((int64_t)layer * a.Hkv + h) * a.T + t) * 128;
-      u32x4 wa = *(const u32x4*)(src + 8 * j), wb = *(const u32x4*)(src + 64 + 8 * j);
-      if (is_k) {
+  for (int base = 0; base < total; base += 128) {
+    u32x4 wa[4], wb[4];
+    uint16_t* dst[4];
+    int rr[4];
+    bool ok[4], rot[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = base + 32 * u + r0;
+      const int r = idx % kRsTok, kind = idx / kRsTok;  // kind: [0, Hkv) K, [Hkv, 2 Hkv) V, then Q heads
+      const int t0 = idx < total ? tok_of[r] : -1;
+      ok[u] = t0 >= 0;
+      const int t = ok[u] ? t0 : (int)a.cs1;  // (addresses of skipped rows are formed but never used)
+      rr[u] = r;
+      rot[u] = kind < a.Hkv || kind >= 2 * a.Hkv;
+      const uint16_t* src;
+      if (kind < 2 * a.Hkv) {
+        const bool is_k = kind < a.Hkv;
+        const int h = is_k ? kind : kind - a.Hkv;
+        src = (is_k ? a.k_pre : a.v_new) + (((int64_t)layer * a.Hkv + h) * a.n + (t - a.cs1)) * 128;
+        dst[u] = (is_k ? a.k : a.v) + (((int64_t)layer * a.Hkv + h) * a.T + t) * 128;
+      } else {
+        const int h = kind - 2 * a.Hkv;
+        src = a.q_pre + (((int64_t)layer * a.Hq + h) * a.n + (t - a.cs1)) * 128;
+        dst[u] = a.q_ws + (((int64_t)blockIdx.y * a.Hq + h) * a.n_sel + m0 + r) * 128;
+      }
+      if (ok[u]) {
+        wa[u] = *(const u32x4*)(src + 8 * j);
+        wb[u] = *(const u32x4*)(src + 64 + 8 * j);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (!ok[u]) continue;
+      if (rot[u]) {
         float cs_[8], sn_[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float2 c = tab[r * kRsTabW + 8 * j + e];
+          const float2 c = tab[rr[u] * kRsTabW + 8 * j + e];
           cs_[e] = c.x;
           sn_[e] = c.y;
         }
-        rotate8(wa, wb, cs_, sn_);
+        rotate8(wa[u], wb[u], cs_, sn_);
       }
-      *(u32x4*)(dst + 8 * j) = wa;
-      *(u32x4*)(dst + 64 + 8 * j) = wb;
-    } else {
-      const int h = kind - 2 * a.Hkv;
-      const uint16_t* src = a.q_pre + (((int64_t)layer * a.Hq + h) * a.n + src_row) * 128;
-      uint16_t* dst = a.q_ws + (((int64_t)blockIdx.y * a.Hq + h) * a.n_sel + m0 + r) * 128;
-      u32x4 wa = *(const u32x4*)(src + 8 * j), wb = *(const u32x4*)(src + 64 + 8 * j);
-      float cs_[8], sn_[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float2 c = tab[r * kRsTabW + 8 * j + e];
-        cs_[e] = c.x;
-        sn_[e] = c.y;
-      }
-      rotate8(wa, wb, cs_, sn_);
-      *(u32x4*)(dst + 8 * j) = wa;
-      *(u32x4*)(dst + 64 + 8 * j) = wb;
+      *(u32x4*)(dst[u] + 8 * j) = wa[u];
+      *(u32x4*)(dst[u] + 64 + 8 * j) = wb[u];
     }
   }
 }
