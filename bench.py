@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--fused-rope-steps", type=int, default=3,
                    help="steps also timed through selective_attend_scatter_rope (pre-rotary fresh rows, "
                         "rotated at the global coordinates; 0: skip)")
+    p.add_argument("--paged-steps", type=int, default=3,
+                   help="steps also timed on the cache held as one buffer per chunk (0: skip)")
     p.add_argument("--batched-steps", type=int, default=3,
                    help="steps also timed with one batched attention call over all layers (0: skip)")
     p.add_argument("--sweep", choices=("none", "rebase", "attention"), default="none",
@@ -107,8 +109,15 @@ def busy_gpu(torch):
     torch.cuda._sleep(400_000)
 
 
-def run_compose(inp, w, rho, binding, torch, out, lse, sel, scores, ws, batched, fused=False):
+def run_compose(inp, w, rho, binding, torch, out, lse, sel, scores, ws, batched, fused=False, paged=False):
     b = binding
+    if paged:   # the same composition on the cache held as one buffer per chunk
+        b.compose_rebase_k_paged(inp.geo, inp.Kc, inp.offsets)
+        k = b.score_deviation_topk_paged(inp.geo, inp.Kc, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
+        for layer in range(w.n_layers):
+            b.selective_attend_scatter_paged(inp.geo, inp.Kc, inp.Vc, layer, layer + 1, sel, k, inp.QF, inp.KF,
+                                             inp.VF, out, lse, ws)
+        return k
     b.compose_rebase_k(inp.geo, inp.K, inp.offsets)
     k = b.score_deviation_topk(inp.geo, inp.K, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
     if fused:   # QF and KF taken as the pre-rotary fresh rows (N(0, 1) either way)
@@ -155,11 +164,14 @@ def main():
     fused = None
     if args.fused_rope_steps > 0:
         fused = bench_rho(inp, w, rho, args.fused_rope_steps, 1, binding, torch, False, fused=True)
+    paged = None
+    if args.paged_steps > 0:
+        paged = bench_rho(inp, w, rho, args.paged_steps, 1, binding, torch, False, paged=True)
     cpu = cpu_baseline(w, rho) if args.cpu_baseline else None
-    emit(args, w, rho, result, rho1, cpu, other, fused)
+    emit(args, w, rho, result, rho1, cpu, other, fused, paged)
 
 
-def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False):
+def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, paged=False):
     b = binding
     n = w.n_candidates
     scores = torch.empty(n, dtype=torch.float32, device="cuda")
@@ -174,13 +186,25 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False):
     stream = torch.cuda.current_stream()
     log(f"[bench] rho={rho}: n_sel={k}, workspace {ws_bytes / 2**20:.1f} MiB, warmup {warmup}, steps {steps}")
 
+    if paged and not hasattr(inp, "Kc"):
+        # one buffer per chunk ([L, H_kv, len_c, D] each), plus pristine copies to restore from
+        cs = w.chunk_start
+        inp.Kc = [inp.K0[:, :, cs[c]:cs[c + 1]].clone() for c in range(w.n_chunks)]
+        inp.Vc = [inp.V0[:, :, cs[c]:cs[c + 1]].clone() for c in range(w.n_chunks)]
+        inp.K0c = [x.clone() for x in inp.Kc]
+        inp.V0c = [x.clone() for x in inp.Vc]
+
     def restore():
-        inp.K.copy_(inp.K0)
-        inp.V.copy_(inp.V0)
+        if paged:
+            for x, x0 in zip(inp.Kc + inp.Vc, inp.K0c + inp.V0c):
+                x.copy_(x0)
+        else:
+            inp.K.copy_(inp.K0)
+            inp.V.copy_(inp.V0)
 
     for _ in range(warmup):
         restore()
-        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused)
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused, paged)
     torch.cuda.synchronize()
     b.cs_trace_reset()
     times = []
@@ -193,7 +217,7 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False):
         busy_gpu(torch)
         b.cs_trace_enable(True)
         e0.record(stream)
-        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused)
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused, paged)
         e1.record(stream)
         b.cs_trace_enable(False)
         torch.cuda.synchronize()
@@ -399,7 +423,7 @@ def _traffic(kernel):
         return None
 
 
-def emit(args, w, rho, r, rho1, cpu, other=None, fused=None):
+def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None):
     tr = r["trace"]
     steps = r["steps"]
     attn_n, attn_ms = tr.get("sel_attn_mfma", (0, 0.0))
@@ -464,6 +488,12 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None):
         fr = fused["trace"].get("rope_scatter_bf16_d128")
         if fr:
             line["fused_rope_scatter_us_per_layer"] = round(fr[1] / fr[0] * 1e3, 2)
+    if paged is not None:
+        line["paged_compose_ms"] = round(paged["ms"], 4)
+        pt = paged["trace"]
+        for key, name in (("paged_sel_attn_us", "sel_attn_mfma"), ("paged_rebase_us", "rebase_bf16_d128")):
+            if name in pt:
+                line[key] = round(pt[name][1] / pt[name][0] * 1e3, 2)
     if rho1 is not None:
         line["rho1_compose_ms"] = round(rho1["ms"], 3)
         line["rho1_over_rho_speedup"] = round(rho1["ms"] / r["ms"], 3)

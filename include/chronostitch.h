@@ -29,7 +29,8 @@
  *  - Tensor layouts are dense, row-major, with the last index contiguous:
  *      caches      [L][H_kv][T][D]   chunks are contiguous token ranges, so
  *                                    the concatenation of the chunk caches is
- *                                    the layout itself
+ *                                    the layout itself (the *_paged calls
+ *                                    take one buffer per chunk instead)
  *      fresh Q     [L][H_q][n][D]    row r <-> token chunk_start[1] + r
  *      fresh K, V  [L][H_kv][n][D]   row r <-> token chunk_start[1] + r
  *    where n = T - chunk_start[1] is the number of later-chunk tokens.
@@ -244,6 +245,53 @@ cs_status selective_attend_scatter(const cs_geometry* g, void* k_cache,
                                    const void* k_fresh, const void* v_fresh,
                                    void* out, float* lse, void* workspace,
                                    size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Paged cache (Section 2: every chunk is prefilled and stored on its own, and
+ * the stored caches are concatenated after re-basing, the step listed after
+ * Eq. 6).  The *_paged calls
+ * take the cache as the chunks' own buffers instead of one composed buffer,
+ * so chunks loaded from storage are used where they landed:
+ *   k_chunks, v_chunks   HOST arrays of geometry.n_chunks DEVICE pointers;
+ *                        chunk c's keys (values) are [L][H_kv][len_c][D],
+ *                        len_c = chunk_start[c+1] - chunk_start[c], dense,
+ *                        row-major.  The arrays are read before the call
+ *                        returns; the buffers are used in place.
+ * Every other argument, the workspace sizes (the contiguous *_workspace
+ * queries apply), the outputs and the errors are those of the contiguous call
+ * of the same name, and the results are bit-identical to that call on the
+ * concatenation of the chunks.
+ * Limits: n_chunks <= 128 when dtype is CS_BF16 and head_dim is 128, <= 64
+ * otherwise (else CS_ERR_UNSUPPORTED).  The attention calls on the bf16 /
+ * head_dim 128 path read whole 64-key tiles from one chunk, so they need every
+ * chunk_start to be a multiple of 64 (else CS_ERR_UNSUPPORTED).  A NULL array
+ * or NULL chunk pointer is CS_ERR_INVALID_ARGUMENT.                          */
+cs_status compose_rebase_k_paged(const cs_geometry* g, void* const* k_chunks,
+                                 const int32_t* chunk_offsets,
+                                 const int32_t* local_coords,
+                                 int32_t* global_coords, void* stream);
+cs_status compose_rebase_k_tokens_paged(const cs_geometry* g, void* const* k_chunks,
+                                        const int32_t* token_offsets, void* stream);
+cs_status score_deviation_topk_paged(const cs_geometry* g, void* const* k_chunks,
+                                     int32_t score_layer, const void* k_fresh,
+                                     double rho, float* scores, int32_t* sel_idx,
+                                     int64_t* n_sel, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+cs_status selective_attend_scatter_paged(const cs_geometry* g, void* const* k_chunks,
+                                         void* const* v_chunks, int32_t layer_begin,
+                                         int32_t layer_end, const int32_t* sel_idx,
+                                         int64_t n_sel, const void* q_fresh,
+                                         const void* k_fresh, const void* v_fresh,
+                                         void* out, float* lse, void* workspace,
+                                         size_t workspace_bytes, void* stream);
+cs_status selective_attend_scatter_rope_paged(const cs_geometry* g, void* const* k_chunks,
+                                              void* const* v_chunks, int32_t layer_begin,
+                                              int32_t layer_end, const int32_t* sel_idx,
+                                              int64_t n_sel, const void* q_pre,
+                                              const void* k_pre, const void* v_fresh,
+                                              const int32_t* coords, void* out, float* lse,
+                                              void* workspace, size_t workspace_bytes,
+                                              void* stream);
 
 /* Thread-local text describing the last non-OK status on this thread. */
 const char* cs_last_error(void);

@@ -59,6 +59,14 @@ def lib():
                                                     vp, sz, vp]
         L.selective_attend_scatter.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp,
                                                vp, sz, vp]
+        L.compose_rebase_k_paged.argtypes = [G, vp, vp, vp, vp, vp]
+        L.compose_rebase_k_tokens_paged.argtypes = [G, vp, vp, vp]
+        L.score_deviation_topk_paged.argtypes = [G, vp, i32, vp, ctypes.c_double, vp, vp,
+                                                 ctypes.POINTER(i64), vp, sz, vp]
+        L.selective_attend_scatter_paged.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp,
+                                                     vp, sz, vp]
+        L.selective_attend_scatter_rope_paged.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp,
+                                                          vp, vp, sz, vp]
         L.cs_last_error.restype = ctypes.c_char_p
         L.cs_trace_enable.argtypes = [i32]
         L.cs_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(i64),
@@ -68,6 +76,8 @@ def lib():
                      "score_deviation_topk",
                      "selective_attend_scatter_workspace", "selective_attend_scatter",
                      "selective_attend_scatter_rope_workspace", "selective_attend_scatter_rope",
+                     "compose_rebase_k_paged", "compose_rebase_k_tokens_paged", "score_deviation_topk_paged",
+                     "selective_attend_scatter_paged", "selective_attend_scatter_rope_paged",
                      "cs_trace_enable", "cs_trace_collect", "cs_trace_get"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -207,3 +217,57 @@ def selective_attend_scatter_rope(geo, k_cache, v_cache, layer_begin, layer_end,
                                                int(layer_end), _ptr(sel_idx), int(n_sel), _ptr(q_pre), _ptr(k_pre),
                                                _ptr(v_fresh), _ptr(coords), _ptr(out), _ptr(lse), _ptr(workspace),
                                                ws_bytes, _stream(stream)))
+
+
+# ---------------------------------------------------------------- paged cache
+def _chunks(ts):
+    """HOST array of the chunk tensors' device pointers (None stays NULL)."""
+    if ts is None:
+        return None
+    arr = (ctypes.c_void_p * max(1, len(ts)))(*[None if t is None else t.data_ptr() for t in ts])
+    return arr
+
+
+def compose_rebase_k_paged(geo, k_chunks, chunk_offsets, local_coords=None, want_global=False, stream=None):
+    """compose_rebase_k on a cache held as one tensor per chunk ([L, H_kv, len_c, D] each)."""
+    off = np.ascontiguousarray(chunk_offsets, dtype=np.int32)
+    loc = None if local_coords is None else np.ascontiguousarray(local_coords, dtype=np.int32)
+    glob = np.empty_like(loc) if (want_global and loc is not None) else None
+    _check(lib().compose_rebase_k_paged(geo.ref, _chunks(k_chunks), off.ctypes.data_as(ctypes.c_void_p),
+                                        None if loc is None else loc.ctypes.data_as(ctypes.c_void_p),
+                                        None if glob is None else glob.ctypes.data_as(ctypes.c_void_p),
+                                        _stream(stream)))
+    return glob
+
+
+def compose_rebase_k_tokens_paged(geo, k_chunks, token_offsets, stream=None):
+    _check(lib().compose_rebase_k_tokens_paged(geo.ref, _chunks(k_chunks), _ptr(token_offsets), _stream(stream)))
+
+
+def score_deviation_topk_paged(geo, k_chunks, score_layer, k_fresh, rho, scores, sel_idx, workspace=None,
+                               stream=None):
+    k = ctypes.c_int64(0)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().score_deviation_topk_paged(geo.ref, _chunks(k_chunks), int(score_layer), _ptr(k_fresh),
+                                            float(rho), _ptr(scores), _ptr(sel_idx), ctypes.byref(k),
+                                            _ptr(workspace), ws_bytes, _stream(stream)))
+    return k.value
+
+
+def selective_attend_scatter_paged(geo, k_chunks, v_chunks, layer_begin, layer_end, sel_idx, n_sel, q_fresh,
+                                   k_fresh, v_fresh, out, lse=None, workspace=None, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().selective_attend_scatter_paged(geo.ref, _chunks(k_chunks), _chunks(v_chunks), int(layer_begin),
+                                                int(layer_end), _ptr(sel_idx), int(n_sel), _ptr(q_fresh),
+                                                _ptr(k_fresh), _ptr(v_fresh), _ptr(out), _ptr(lse),
+                                                _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def selective_attend_scatter_rope_paged(geo, k_chunks, v_chunks, layer_begin, layer_end, sel_idx, n_sel, q_pre,
+                                        k_pre, v_fresh, coords, out, lse=None, workspace=None, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().selective_attend_scatter_rope_paged(geo.ref, _chunks(k_chunks), _chunks(v_chunks),
+                                                     int(layer_begin), int(layer_end), _ptr(sel_idx), int(n_sel),
+                                                     _ptr(q_pre), _ptr(k_pre), _ptr(v_fresh), _ptr(coords),
+                                                     _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes,
+                                                     _stream(stream)))

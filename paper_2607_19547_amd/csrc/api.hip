@@ -121,6 +121,144 @@ int64_t n_select(double rho, int64_t n) {
 
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+static CacheView flat_view(void* k, void* v) {
+  CacheView cv;
+  cv.k = k;
+  cv.v = v;
+  return cv;
+}
+
+// A paged cache: n_chunks device pointers per tensor (v_chunks only when
+// the call writes or reads values).
+static cs_status paged_view(const Geo& g, void* const* k_chunks, void* const* v_chunks, bool need_v,
+                            CacheView* cv) {
+  const int cap = g.dtype == CS_BF16 && g.D == 128 ? kMaxPages : kMaxPagesGeneric;
+  if (g.N > cap)
+    return fail(CS_ERR_UNSUPPORTED, "a paged cache holds at most " + std::to_string(cap) + " chunks");
+  if (!k_chunks || (need_v && !v_chunks)) return fail(CS_ERR_INVALID_ARGUMENT, "chunk pointer array is NULL");
+  for (int c = 0; c < g.N; ++c)
+    if (!k_chunks[c] || (need_v && !v_chunks[c]))
+      return fail(CS_ERR_INVALID_ARGUMENT, "chunk " + std::to_string(c) + " has a NULL buffer");
+  cv->paged = true;
+  cv->k_chunks = k_chunks;
+  cv->v_chunks = need_v ? v_chunks : nullptr;
+  return CS_OK;
+}
+
+static cs_status theta_table(const cs_geometry* gp, const Geo& g, std::vector<double>* theta) {
+  theta->resize(g.P);
+  for (int i = 0; i < g.P; ++i)
+    (*theta)[i] = gp->inv_freq ? gp->inv_freq[i] : pow(gp->rope_base, -2.0 * i / (double)g.D);
+  for (int i = 0; i < g.P; ++i)
+    if (!isfinite((*theta)[i])) return fail(CS_ERR_INVALID_ARGUMENT, "inv_freq holds a non-finite value");
+  return CS_OK;
+}
+
+// ------------------------------------------------------------------ calls on either layout
+static cs_status rebase_k(const cs_geometry* gp, const Geo& g, const CacheView& cv, const int32_t* chunk_offsets,
+                          const int32_t* local_coords, int32_t* global_coords, void* stream) {
+  if (!chunk_offsets) return fail(CS_ERR_INVALID_ARGUMENT, "chunk_offsets is NULL");
+  if (global_coords && !local_coords)
+    return fail(CS_ERR_INVALID_ARGUMENT, "global_coords needs local_coords");
+  std::vector<double> theta;
+  cs_status st = theta_table(gp, g, &theta);
+  if (st) return st;
+  // Coordinate shift (host): p' = p + Delta_c for every token of chunk c.
+  if (global_coords) {
+    for (int c = 0; c < g.N; ++c)
+      for (int64_t t = g.cs[c]; t < g.cs[c + 1]; ++t)
+        for (int a = 0; a < 3; ++a)
+          global_coords[3 * t + a] = local_coords[3 * t + a] + chunk_offsets[3 * c + a];
+  }
+  return launch_rebase(g, cv, chunk_offsets, theta.data(), (hipStream_t)stream);
+}
+
+static cs_status rebase_k_tokens(const cs_geometry* gp, const Geo& g, const CacheView& cv,
+                                 const int32_t* token_offsets, void* stream) {
+  if (!token_offsets) return fail(CS_ERR_INVALID_ARGUMENT, "token_offsets is NULL");
+  std::vector<double> theta;
+  cs_status st = theta_table(gp, g, &theta);
+  if (st) return st;
+  return launch_rebase_tokens(g, cv, token_offsets, theta.data(), (hipStream_t)stream);
+}
+
+static cs_status score_topk(const Geo& g, const CacheView& cv, int32_t score_layer, const void* k_fresh, double rho,
+                            float* scores, int32_t* sel_idx, int64_t* n_sel, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  if (!n_sel) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel is NULL");
+  if (!(rho >= 0.0 && rho <= 1.0)) return fail(CS_ERR_INVALID_ARGUMENT, "rho must lie in [0, 1]");
+  if (score_layer < 0 || score_layer >= g.L)
+    return fail(CS_ERR_INVALID_ARGUMENT, "score_layer out of range");
+  int64_t k = n_select(rho, g.n);
+  if (g.n > 0) {
+    if ((!cv.paged && !cv.k) || !k_fresh) return fail(CS_ERR_INVALID_ARGUMENT, "k_cache or k_fresh is NULL");
+    if (k > 0 && !sel_idx) return fail(CS_ERR_INVALID_ARGUMENT, "sel_idx is NULL");
+    if (!scores) {
+      size_t need = align_up((size_t)g.n * sizeof(float), 256);
+      if (!workspace || workspace_bytes < need)
+        return fail(CS_ERR_WORKSPACE_TOO_SMALL, "workspace must hold n float32 scores when scores is NULL");
+      scores = (float*)workspace;
+    }
+  }
+  *n_sel = k;
+  if (g.n == 0) return CS_OK;
+  return launch_score_select(g, cv, score_layer, k_fresh, scores, sel_idx, k, (hipStream_t)stream);
+}
+
+static cs_status attend_scatter(const Geo& g, const CacheView& cv, int32_t layer_begin, int32_t layer_end,
+                                const int32_t* sel_idx, int64_t n_sel, const void* q_fresh, const void* k_fresh,
+                                const void* v_fresh, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  if (!sel_idx || !q_fresh || !k_fresh || !v_fresh || !out)
+    return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  AttnPlan p = plan_attention(g, n_sel, layer_end - layer_begin);
+  size_t need = p.mfma ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)(layer_end - layer_begin) : 0;
+  if (need && (!workspace || workspace_bytes < need))
+    return fail(CS_ERR_WORKSPACE_TOO_SMALL,
+                "workspace smaller than selective_attend_scatter_workspace() (" + std::to_string(need) +
+                    " bytes)");
+  if (cv.paged && p.mfma && !chunks_tile_aligned(g))
+    return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
+  hipStream_t s = (hipStream_t)stream;
+  cs_status st = launch_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, k_fresh, v_fresh, s);
+  if (st) return st;
+  return launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, false, out, lse, workspace, s);
+}
+
+// Workspace of the fused-rotary variant: the attention's, then the rotated
+// queries [layers in call][H_q][n_sel][D].
+static size_t rope_ws(const Geo& g, const AttnPlan& p, int64_t n_sel, int layers, size_t* att_bytes) {
+  const size_t att = p.mfma && n_sel > 0 && layers > 0 ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)layers : 0;
+  *att_bytes = align_up(att, 256);
+  return *att_bytes + (size_t)layers * g.Hq * n_sel * g.D * g.esize;
+}
+
+static cs_status attend_scatter_rope(const cs_geometry* gp, const Geo& g, const CacheView& cv, int32_t layer_begin,
+                                     int32_t layer_end, const int32_t* sel_idx, int64_t n_sel, const void* q_pre,
+                                     const void* k_pre, const void* v_fresh, const int32_t* coords, void* out,
+                                     float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!sel_idx || !q_pre || !k_pre || !v_fresh || !coords || !out)
+    return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  std::vector<double> theta;
+  cs_status st = theta_table(gp, g, &theta);
+  if (st) return st;
+  const int layers = layer_end - layer_begin;
+  AttnPlan p = plan_attention(g, n_sel, layers);
+  size_t att = 0;
+  const size_t need = rope_ws(g, p, n_sel, layers, &att);
+  if (!workspace || workspace_bytes < need)
+    return fail(CS_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than selective_attend_scatter_rope_workspace() (" +
+                                                std::to_string(need) + " bytes)");
+  if (cv.paged && p.mfma && !chunks_tile_aligned(g))
+    return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
+  hipStream_t s = (hipStream_t)stream;
+  void* q_ws = (char*)workspace + att;
+  st = launch_rope_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords, theta.data(),
+                           q_ws, s);
+  if (st) return st;
+  return launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_ws, true, out, lse, workspace, s);
+}
+
 }  // namespace cs
 
 using namespace cs;
@@ -136,23 +274,18 @@ cs_status compose_rebase_k(const cs_geometry* gp, void* k_cache, const int32_t* 
   cs_status st = check_geometry(gp, &g);
   if (st) return st;
   if (!k_cache) return fail(CS_ERR_INVALID_ARGUMENT, "k_cache is NULL");
-  if (!chunk_offsets) return fail(CS_ERR_INVALID_ARGUMENT, "chunk_offsets is NULL");
-  if (global_coords && !local_coords)
-    return fail(CS_ERR_INVALID_ARGUMENT, "global_coords needs local_coords");
-  // Coordinate shift (host): p' = p + Delta_c for every token of chunk c.
-  if (global_coords) {
-    for (int c = 0; c < g.N; ++c)
-      for (int64_t t = g.cs[c]; t < g.cs[c + 1]; ++t)
-        for (int a = 0; a < 3; ++a)
-          global_coords[3 * t + a] = local_coords[3 * t + a] + chunk_offsets[3 * c + a];
-  }
-  // theta_i in float64 (host): the caller's table or base^(-2i/D).
-  std::vector<double> theta(g.P);
-  for (int i = 0; i < g.P; ++i)
-    theta[i] = gp->inv_freq ? gp->inv_freq[i] : pow(gp->rope_base, -2.0 * i / (double)g.D);
-  for (int i = 0; i < g.P; ++i)
-    if (!isfinite(theta[i])) return fail(CS_ERR_INVALID_ARGUMENT, "inv_freq holds a non-finite value");
-  return launch_rebase(g, k_cache, chunk_offsets, theta.data(), (hipStream_t)stream);
+  return rebase_k(gp, g, flat_view(k_cache, nullptr), chunk_offsets, local_coords, global_coords, stream);
+}
+
+cs_status compose_rebase_k_paged(const cs_geometry* gp, void* const* k_chunks, const int32_t* chunk_offsets,
+                                 const int32_t* local_coords, int32_t* global_coords, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  CacheView cv;
+  st = paged_view(g, k_chunks, nullptr, false, &cv);
+  if (st) return st;
+  return rebase_k(gp, g, cv, chunk_offsets, local_coords, global_coords, stream);
 }
 
 cs_status compose_rebase_k_tokens(const cs_geometry* gp, void* k_cache, const int32_t* token_offsets,
@@ -161,13 +294,18 @@ cs_status compose_rebase_k_tokens(const cs_geometry* gp, void* k_cache, const in
   cs_status st = check_geometry(gp, &g);
   if (st) return st;
   if (!k_cache) return fail(CS_ERR_INVALID_ARGUMENT, "k_cache is NULL");
-  if (!token_offsets) return fail(CS_ERR_INVALID_ARGUMENT, "token_offsets is NULL");
-  std::vector<double> theta(g.P);
-  for (int i = 0; i < g.P; ++i)
-    theta[i] = gp->inv_freq ? gp->inv_freq[i] : pow(gp->rope_base, -2.0 * i / (double)g.D);
-  for (int i = 0; i < g.P; ++i)
-    if (!isfinite(theta[i])) return fail(CS_ERR_INVALID_ARGUMENT, "inv_freq holds a non-finite value");
-  return launch_rebase_tokens(g, k_cache, token_offsets, theta.data(), (hipStream_t)stream);
+  return rebase_k_tokens(gp, g, flat_view(k_cache, nullptr), token_offsets, stream);
+}
+
+cs_status compose_rebase_k_tokens_paged(const cs_geometry* gp, void* const* k_chunks, const int32_t* token_offsets,
+                                        void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  CacheView cv;
+  st = paged_view(g, k_chunks, nullptr, false, &cv);
+  if (st) return st;
+  return rebase_k_tokens(gp, g, cv, token_offsets, stream);
 }
 
 cs_status score_deviation_topk_workspace(const cs_geometry* gp, size_t* bytes) {
@@ -186,25 +324,20 @@ cs_status score_deviation_topk(const cs_geometry* gp, const void* k_cache, int32
   Geo g;
   cs_status st = check_geometry(gp, &g);
   if (st) return st;
-  if (!n_sel) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel is NULL");
-  if (!(rho >= 0.0 && rho <= 1.0)) return fail(CS_ERR_INVALID_ARGUMENT, "rho must lie in [0, 1]");
-  if (score_layer < 0 || score_layer >= g.L)
-    return fail(CS_ERR_INVALID_ARGUMENT, "score_layer out of range");
-  int64_t k = n_select(rho, g.n);
-  if (g.n > 0) {
-    if (!k_cache || !k_fresh) return fail(CS_ERR_INVALID_ARGUMENT, "k_cache or k_fresh is NULL");
-    if (k > 0 && !sel_idx) return fail(CS_ERR_INVALID_ARGUMENT, "sel_idx is NULL");
-    if (!scores) {
-      size_t need = align_up((size_t)g.n * sizeof(float), 256);
-      if (!workspace || workspace_bytes < need)
-        return fail(CS_ERR_WORKSPACE_TOO_SMALL, "workspace must hold n float32 scores when scores is NULL");
-      scores = (float*)workspace;
-    }
-  }
-  *n_sel = k;
-  if (g.n == 0) return CS_OK;
-  const char* kl = (const char*)k_cache + (size_t)score_layer * g.Hkv * g.T * g.D * g.esize;
-  return launch_score_select(g, kl, k_fresh, scores, sel_idx, k, (hipStream_t)stream);
+  return score_topk(g, flat_view((void*)k_cache, nullptr), score_layer, k_fresh, rho, scores, sel_idx, n_sel,
+                    workspace, workspace_bytes, stream);
+}
+
+cs_status score_deviation_topk_paged(const cs_geometry* gp, void* const* k_chunks, int32_t score_layer,
+                                     const void* k_fresh, double rho, float* scores, int32_t* sel_idx,
+                                     int64_t* n_sel, void* workspace, size_t workspace_bytes, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  CacheView cv;
+  st = paged_view(g, k_chunks, nullptr, false, &cv);
+  if (st) return st;
+  return score_topk(g, cv, score_layer, k_fresh, rho, scores, sel_idx, n_sel, workspace, workspace_bytes, stream);
 }
 
 cs_status selective_attend_scatter_workspace(const cs_geometry* gp, int64_t n_sel,
@@ -223,6 +356,13 @@ cs_status selective_attend_scatter_workspace(const cs_geometry* gp, int64_t n_se
   return CS_OK;
 }
 
+static cs_status check_layers(const Geo& g, int32_t layer_begin, int32_t layer_end, int64_t n_sel) {
+  if (layer_begin < 0 || layer_end < layer_begin || layer_end > g.L)
+    return fail(CS_ERR_INVALID_ARGUMENT, "need 0 <= layer_begin <= layer_end <= n_layers");
+  if (n_sel < 0 || n_sel > g.n) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel must be in [0, n]");
+  return CS_OK;
+}
+
 cs_status selective_attend_scatter(const cs_geometry* gp, void* k_cache, void* v_cache,
                                    int32_t layer_begin, int32_t layer_end, const int32_t* sel_idx,
                                    int64_t n_sel, const void* q_fresh, const void* k_fresh,
@@ -230,32 +370,29 @@ cs_status selective_attend_scatter(const cs_geometry* gp, void* k_cache, void* v
                                    size_t workspace_bytes, void* stream) {
   Geo g;
   cs_status st = check_geometry(gp, &g);
+  if (!st) st = check_layers(g, layer_begin, layer_end, n_sel);
   if (st) return st;
-  if (layer_begin < 0 || layer_end < layer_begin || layer_end > g.L)
-    return fail(CS_ERR_INVALID_ARGUMENT, "need 0 <= layer_begin <= layer_end <= n_layers");
-  if (n_sel < 0 || n_sel > g.n) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel must be in [0, n]");
   if (n_sel == 0 || layer_end == layer_begin) return CS_OK;
-  if (!k_cache || !v_cache || !sel_idx || !q_fresh || !k_fresh || !v_fresh || !out)
-    return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
-  AttnPlan p = plan_attention(g, n_sel, layer_end - layer_begin);
-  size_t need = p.mfma ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)(layer_end - layer_begin) : 0;
-  if (need && (!workspace || workspace_bytes < need))
-    return fail(CS_ERR_WORKSPACE_TOO_SMALL,
-                "workspace smaller than selective_attend_scatter_workspace() (" + std::to_string(need) +
-                    " bytes)");
-  hipStream_t s = (hipStream_t)stream;
-  st = launch_scatter(g, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, k_fresh, v_fresh, s);
-  if (st) return st;
-  return launch_attention(g, p, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_fresh, false,
-                          out, lse, workspace, s);
+  if (!k_cache || !v_cache) return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  return attend_scatter(g, flat_view(k_cache, v_cache), layer_begin, layer_end, sel_idx, n_sel, q_fresh, k_fresh,
+                        v_fresh, out, lse, workspace, workspace_bytes, stream);
 }
 
-// Workspace of the fused-rotary variant: the attention's, then the rotated
-// queries [layers in call][H_q][n_sel][D].
-static size_t rope_ws(const Geo& g, const AttnPlan& p, int64_t n_sel, int layers, size_t* att_bytes) {
-  const size_t att = p.mfma && n_sel > 0 && layers > 0 ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)layers : 0;
-  *att_bytes = align_up(att, 256);
-  return *att_bytes + (size_t)layers * g.Hq * n_sel * g.D * g.esize;
+cs_status selective_attend_scatter_paged(const cs_geometry* gp, void* const* k_chunks, void* const* v_chunks,
+                                         int32_t layer_begin, int32_t layer_end, const int32_t* sel_idx,
+                                         int64_t n_sel, const void* q_fresh, const void* k_fresh,
+                                         const void* v_fresh, void* out, float* lse, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (!st) st = check_layers(g, layer_begin, layer_end, n_sel);
+  if (st) return st;
+  if (n_sel == 0 || layer_end == layer_begin) return CS_OK;
+  CacheView cv;
+  st = paged_view(g, k_chunks, v_chunks, true, &cv);
+  if (st) return st;
+  return attend_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, k_fresh, v_fresh, out, lse,
+                        workspace, workspace_bytes, stream);
 }
 
 cs_status selective_attend_scatter_rope_workspace(const cs_geometry* gp, int64_t n_sel, int32_t n_layers_per_call,
@@ -280,32 +417,29 @@ cs_status selective_attend_scatter_rope(const cs_geometry* gp, void* k_cache, vo
                                         size_t workspace_bytes, void* stream) {
   Geo g;
   cs_status st = check_geometry(gp, &g);
+  if (!st) st = check_layers(g, layer_begin, layer_end, n_sel);
   if (st) return st;
-  if (layer_begin < 0 || layer_end < layer_begin || layer_end > g.L)
-    return fail(CS_ERR_INVALID_ARGUMENT, "need 0 <= layer_begin <= layer_end <= n_layers");
-  if (n_sel < 0 || n_sel > g.n) return fail(CS_ERR_INVALID_ARGUMENT, "n_sel must be in [0, n]");
   if (n_sel == 0 || layer_end == layer_begin) return CS_OK;
-  if (!k_cache || !v_cache || !sel_idx || !q_pre || !k_pre || !v_fresh || !coords || !out)
-    return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
-  std::vector<double> theta(g.P);
-  for (int i = 0; i < g.P; ++i)
-    theta[i] = gp->inv_freq ? gp->inv_freq[i] : pow(gp->rope_base, -2.0 * i / (double)g.D);
-  for (int i = 0; i < g.P; ++i)
-    if (!isfinite(theta[i])) return fail(CS_ERR_INVALID_ARGUMENT, "inv_freq holds a non-finite value");
-  const int layers = layer_end - layer_begin;
-  AttnPlan p = plan_attention(g, n_sel, layers);
-  size_t att = 0;
-  const size_t need = rope_ws(g, p, n_sel, layers, &att);
-  if (!workspace || workspace_bytes < need)
-    return fail(CS_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than selective_attend_scatter_rope_workspace() (" +
-                                                std::to_string(need) + " bytes)");
-  hipStream_t s = (hipStream_t)stream;
-  void* q_ws = (char*)workspace + att;
-  st = launch_rope_scatter(g, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords,
-                           theta.data(), q_ws, s);
+  if (!k_cache || !v_cache) return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  return attend_scatter_rope(gp, g, flat_view(k_cache, v_cache), layer_begin, layer_end, sel_idx, n_sel, q_pre,
+                             k_pre, v_fresh, coords, out, lse, workspace, workspace_bytes, stream);
+}
+
+cs_status selective_attend_scatter_rope_paged(const cs_geometry* gp, void* const* k_chunks, void* const* v_chunks,
+                                              int32_t layer_begin, int32_t layer_end, const int32_t* sel_idx,
+                                              int64_t n_sel, const void* q_pre, const void* k_pre,
+                                              const void* v_fresh, const int32_t* coords, void* out, float* lse,
+                                              void* workspace, size_t workspace_bytes, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (!st) st = check_layers(g, layer_begin, layer_end, n_sel);
   if (st) return st;
-  return launch_attention(g, p, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_ws, true, out, lse,
-                          workspace, s);
+  if (n_sel == 0 || layer_end == layer_begin) return CS_OK;
+  CacheView cv;
+  st = paged_view(g, k_chunks, v_chunks, true, &cv);
+  if (st) return st;
+  return attend_scatter_rope(gp, g, cv, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords, out,
+                             lse, workspace, workspace_bytes, stream);
 }
 
 // ------------------------------------------------------------------ tracing exports

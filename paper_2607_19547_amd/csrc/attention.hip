@@ -36,14 +36,18 @@
 namespace cs {
 
 // ============================================================== scatter
-__global__ __launch_bounds__(256) void scatter_rows(char* __restrict__ k, char* __restrict__ v,
-                                                    const char* __restrict__ kf,
+// K[layer][h][t] <- K_fresh[layer][h][t - s1] and the same for V, for every
+// selected token t; cache rows are reached through the row map.  W is the
+// bytes one thread moves (16 when a row is a whole number of 16-byte words).
+template <int W, typename Rows>
+__global__ __launch_bounds__(256) void scatter_rows(const Rows rows, const char* __restrict__ kf,
                                                     const char* __restrict__ vf,
                                                     const int32_t* __restrict__ sel, int64_t n_sel,
                                                     int64_t T, int64_t n, int64_t cs1, int Hkv,
                                                     int row_bytes, int lb) {
+  typedef typename std::conditional<W == 16, u32x4, uint32_t>::type word;
   const int layer = lb + blockIdx.y;
-  const int words = row_bytes / 16;
+  const int words = row_bytes / W;
   const int64_t total = (int64_t)Hkv * n_sel * words;
   for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < total;
        w += (int64_t)gridDim.x * blockDim.x) {
@@ -53,50 +57,35 @@ __global__ __launch_bounds__(256) void scatter_rows(char* __restrict__ k, char* 
     const int h = (int)(hm / n_sel);
     const int64_t t = sel[m];
     if (t < cs1 || t >= T) continue;  // out-of-contract index: never write outside the cache
-    const int64_t dst = (((int64_t)layer * Hkv + h) * T + t) * row_bytes + 16 * c;
-    const int64_t src = (((int64_t)layer * Hkv + h) * n + (t - cs1)) * row_bytes + 16 * c;
-    *(u32x4*)(k + dst) = *(const u32x4*)(kf + src);
-    *(u32x4*)(v + dst) = *(const u32x4*)(vf + src);
+    char *kr, *vr;
+    rows.kv_rows((int64_t)layer * Hkv + h, t, row_bytes, kr, vr);
+    const int64_t src = (((int64_t)layer * Hkv + h) * n + (t - cs1)) * row_bytes + W * c;
+    *(word*)(kr + W * c) = *(const word*)(kf + src);
+    *(word*)(vr + W * c) = *(const word*)(vf + src);
   }
 }
 
-__global__ __launch_bounds__(256) void scatter_rows_w4(char* __restrict__ k, char* __restrict__ v,
-                                                       const char* __restrict__ kf,
-                                                       const char* __restrict__ vf,
-                                                       const int32_t* __restrict__ sel, int64_t n_sel,
-                                                       int64_t T, int64_t n, int64_t cs1, int Hkv,
-                                                       int row_bytes, int lb) {
-  const int layer = lb + blockIdx.y;
-  const int words = row_bytes / 4;
-  const int64_t total = (int64_t)Hkv * n_sel * words;
-  for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < total;
-       w += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(w % words);
-    const int64_t hm = w / words;
-    const int64_t m = hm % n_sel;
-    const int h = (int)(hm / n_sel);
-    const int64_t t = sel[m];
-    if (t < cs1 || t >= T) continue;
-    const int64_t dst = (((int64_t)layer * Hkv + h) * T + t) * row_bytes + 4 * c;
-    const int64_t src = (((int64_t)layer * Hkv + h) * n + (t - cs1)) * row_bytes + 4 * c;
-    *(uint32_t*)(k + dst) = *(const uint32_t*)(kf + src);
-    *(uint32_t*)(v + dst) = *(const uint32_t*)(vf + src);
-  }
-}
-
-cs_status launch_scatter(const Geo& g, void* k, void* v, int lb, int le, const int32_t* sel,
-                         int64_t n_sel, const void* kf, const void* vf, hipStream_t s) {
+template <typename Rows>
+static void launch_scatter_rows(const Geo& g, const Rows& rows, int lb, int le, const int32_t* sel, int64_t n_sel,
+                                const void* kf, const void* vf, hipStream_t s) {
+  static_assert(sizeof(Rows) + 96 <= 4096, "kernel arguments within 4 KB");
   const int row_bytes = g.D * g.esize;
   const bool wide = row_bytes % 16 == 0;
   const int64_t total = (int64_t)g.Hkv * n_sel * (wide ? row_bytes / 16 : row_bytes / 4);
   const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 65535);
   TraceScope tr("scatter_rows", s);
   if (wide)
-    hipLaunchKernelGGL(scatter_rows, dim3(blocks, le - lb), dim3(256), 0, s, (char*)k, (char*)v,
-                       (const char*)kf, (const char*)vf, sel, n_sel, g.T, g.n, g.cs1, g.Hkv, row_bytes, lb);
+    hipLaunchKernelGGL((scatter_rows<16, Rows>), dim3(blocks, le - lb), dim3(256), 0, s, rows, (const char*)kf,
+                       (const char*)vf, sel, n_sel, g.T, g.n, g.cs1, g.Hkv, row_bytes, lb);
   else
-    hipLaunchKernelGGL(scatter_rows_w4, dim3(blocks, le - lb), dim3(256), 0, s, (char*)k, (char*)v,
-                       (const char*)kf, (const char*)vf, sel, n_sel, g.T, g.n, g.cs1, g.Hkv, row_bytes, lb);
+    hipLaunchKernelGGL((scatter_rows<4, Rows>), dim3(blocks, le - lb), dim3(256), 0, s, rows, (const char*)kf,
+                       (const char*)vf, sel, n_sel, g.T, g.n, g.cs1, g.Hkv, row_bytes, lb);
+}
+
+cs_status launch_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
+                         const void* kf, const void* vf, hipStream_t s) {
+  if (cv.paged) launch_scatter_rows(g, cv.pages<kMaxPages>(g), lb, le, sel, n_sel, kf, vf, s);
+  else launch_scatter_rows(g, cv.flat(g), lb, le, sel, n_sel, kf, vf, s);
   return check_launch("scatter launch");
 }
 
@@ -112,8 +101,6 @@ constexpr float kRescaleLog2 = 8.0f;     // lazy rescale threshold (max growth 2
 
 struct AttnArgs {
   const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
   const int32_t* sel;
   uint16_t* out;
   float* lse;
@@ -151,8 +138,8 @@ __device__ __forceinline__ float pair_sum(float x) {
 // see that reads of one slot do not wait for DMA into another.
 typedef __attribute__((address_space(3))) void lds_void;
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const uint16_t* base, int64_t T) {
-  return __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, (int)(T * kRow), 0x00020000);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const char* base, int64_t rows) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, (int)(rows * kRow), 0x00020000);
 }
 
 struct StageOffsets {
@@ -367,8 +354,9 @@ __global__ __launch_bounds__(1024) void plan_items(const int32_t* __restrict__ s
   }
 }
 
-template <int G>
-__global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
+template <int G, typename Rows>
+__global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, const Rows rows) {
+  constexpr bool kPaged = !std::is_same<Rows, FlatRows>::value;
   constexpr int RW = 32 / G;       // selected rows per wavefront
   constexpr int RT = kWaves * RW;  // selected rows per workgroup tile
   // The V ring takes the low 64 KB of LDS, where the DS instruction's 16-bit
@@ -493,12 +481,43 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   const int g_wmin = mw0 < a.n_sel ? a.sel[mw0] : 0x7fffffff;
   const int g_wmax = mw0 < a.n_sel ? a.sel[mw1] : -1;
 
-  const __amdgpu_buffer_rsrc_t rk = plane_rsrc(a.k + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
-  const __amdgpu_buffer_rsrc_t rv = plane_rsrc(a.v + ((int64_t)layer * a.Hkv + kv) * a.T * 128, a.T);
+  // Key tiles are fetched in ascending order.  A contiguous cache is one
+  // buffer range per plane; in a paged cache every 64-key tile lies inside
+  // one chunk (chunk starts are multiples of 64), and the range follows the
+  // chunk of the tile being fetched.  Rows past a range read as zeros.
+  const int64_t plane = (int64_t)layer * a.Hkv + kv;
+  __amdgpu_buffer_rsrc_t rk, rv;
+  int dma_c = 0, dma_first = 0, dma_next = 0x7fffffff;
+  auto use_chunk = [&](int c) {
+    if constexpr (kPaged) {
+      const int s0 = rows.start[c], len = rows.start[c + 1] - s0;
+      rk = plane_rsrc(rows.k[c] + plane * len * kRow, len);
+      rv = plane_rsrc(rows.v[c] + plane * len * kRow, len);
+      dma_c = c;
+      dma_first = s0;
+      dma_next = c + 1 < rows.n ? rows.start[c + 1] : 0x7fffffff;
+    }
+  };
+  if constexpr (kPaged) {
+    use_chunk(__builtin_amdgcn_readfirstlane(rows.chunk_of(key_begin)));
+  } else {
+    rk = plane_rsrc(rows.k + plane * a.T * kRow, a.T);
+    rv = plane_rsrc(rows.v + plane * a.T * kRow, a.T);
+  }
+  auto fetch = [&](int kt, char* Kd, char* Vd) {
+    if constexpr (kPaged) {
+      if (kt >= dma_next) {
+        int c = dma_c + 1;
+        while (c + 1 < rows.n && rows.start[c + 1] <= kt) ++c;
+        use_chunk(c);
+      }
+    }
+    stage_dma(rk, rv, so, kt - dma_first, Kd, Vd, wave);
+  };
   const int n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
-  stage_dma(rk, rv, so, key_begin, up_k0, lo_v0, wave);
-  stage_dma(rk, rv, so, key_begin + kKT, up_k1, lo_v1, wave);
-  stage_dma(rk, rv, so, key_begin + 2 * kKT, up_k2, lo_v2, wave);
+  fetch(key_begin, up_k0, lo_v0);
+  fetch(key_begin + kKT, up_k1, lo_v1);
+  fetch(key_begin + 2 * kKT, up_k2, lo_v2);
 
   bf16x8 qb[8];
   if (valid) {
@@ -628,7 +647,7 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a) {
   // A wavefront whose rows all end before tile i skips the arithmetic.
   auto step = [&](auto C, auto N, auto S, int i, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
     const int kt = key_begin + i * kKT;
-    stage_dma(rk, rv, so, kt + 3 * kKT, kbuf(S), vbuf(S), wave);
+    fetch(kt + 3 * kKT, kbuf(S), vbuf(S));
     if (kt <= g_wmax) {
       qk_head(N, n0, n1);
       mask_max(kt, c0, c1);
@@ -755,8 +774,6 @@ __global__ __launch_bounds__(256) void sel_attn_combine(const AttnArgs a) {
 // ============================================================== generic attention
 struct GenAttnArgs {
   const void* q;
-  const void* k;
-  const void* v;
   const int32_t* sel;
   void* out;
   float* lse;
@@ -790,8 +807,8 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-template <typename E>
-__global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a) {
+template <typename E, typename Rows>
+__global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a, const Rows rows) {
   __shared__ float qs[512];
   __shared__ float ps[64];
   const int64_t m = blockIdx.x;
@@ -803,8 +820,8 @@ __global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a) {
   const int kv = h / a.G;
   const E* qp = (const E*)a.q + (a.q_by_slot ? ((int64_t)blockIdx.z * a.Hq + h) * a.n_sel + m
                                              : ((int64_t)layer * a.Hq + h) * a.n + (t - a.cs1)) * a.D;
-  const E* kb = (const E*)a.k + ((int64_t)layer * a.Hkv + kv) * a.T * a.D;
-  const E* vb = (const E*)a.v + ((int64_t)layer * a.Hkv + kv) * a.T * a.D;
+  const int64_t plane = (int64_t)layer * a.Hkv + kv;
+  const int rb = a.D * (int)sizeof(E);
   for (int d = lane; d < a.D; d += 64) qs[d] = gld(qp + d);
   __syncthreads();
   float acc[8];
@@ -815,7 +832,7 @@ __global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a) {
     const int j = j0 + lane;
     float s = -INFINITY;
     if (j <= t) {
-      const E* kr = kb + (int64_t)j * a.D;
+      const E* kr = (const E*)rows.row(false, plane, j, rb);
       float dot = 0.f;
       for (int d = 0; d < a.D; ++d) dot = fmaf(qs[d], gld(kr + d), dot);
       s = dot * a.scale;
@@ -831,7 +848,7 @@ __global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a) {
     const int cnt = min(64, t + 1 - j0);
     for (int jj = 0; jj < cnt; ++jj) {
       const float pj = ps[jj];
-      const E* vr = vb + (int64_t)(j0 + jj) * a.D;
+      const E* vr = (const E*)rows.row(true, plane, j0 + jj, rb);
 #pragma unroll
       for (int x = 0; x < 8; ++x) {
         const int d = lane + 64 * x;
@@ -884,8 +901,9 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call) {
   return p;
 }
 
-template <int G>
-static void launch_mfma_g(const AttnArgs& a, hipStream_t s) {
+template <int G, typename Rows>
+static void launch_mfma_g(const AttnArgs& a, const Rows& rows, hipStream_t s) {
+  static_assert(sizeof(AttnArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
   {
     TraceScope tr("plan_items", s);
     hipLaunchKernelGGL(plan_items, dim3(1), dim3(1024), 0, s, a.sel, a.n_sel, a.n_tiles, kWaves * (32 / G), a.T,
@@ -899,7 +917,7 @@ static void launch_mfma_g(const AttnArgs& a, hipStream_t s) {
     const int64_t per_q = (a.n_tiles * a.Hkv + a.part_cap + nq - 1) / nq;
     const int64_t share = kXcds / nq;
     const int64_t grid = (per_q * a.layers + share - 1) / share * kXcds;
-    hipLaunchKernelGGL(sel_attn_mfma<G>, dim3((unsigned)grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((sel_attn_mfma<G, Rows>), dim3((unsigned)grid), dim3(kThreads), 0, s, a, rows);
   }
   if (a.part_cap > 0) {
     // cut row tiles lead the longest-first order, and each fills at least
@@ -910,15 +928,48 @@ static void launch_mfma_g(const AttnArgs& a, hipStream_t s) {
   }
 }
 
-cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const void* v, int lb, int le,
+template <typename Rows>
+static cs_status launch_mfma(int G, const AttnArgs& a, const Rows& rows, hipStream_t s) {
+  switch (G) {
+    case 1: launch_mfma_g<1>(a, rows, s); break;
+    case 2: launch_mfma_g<2>(a, rows, s); break;
+    case 4: launch_mfma_g<4>(a, rows, s); break;
+    case 8: launch_mfma_g<8>(a, rows, s); break;
+    case 16: launch_mfma_g<16>(a, rows, s); break;
+    case 32: launch_mfma_g<32>(a, rows, s); break;
+    default: return fail(CS_ERR_UNSUPPORTED, "MFMA attention needs H_q/H_kv dividing 32");
+  }
+  return CS_OK;
+}
+
+template <typename Rows>
+static void launch_generic(const Geo& g, const GenAttnArgs& a, const Rows& rows, int64_t n_sel, int layers,
+                           hipStream_t s) {
+  static_assert(sizeof(GenAttnArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
+  TraceScope tr("sel_attn_generic", s);
+  if (g.dtype == CS_BF16)
+    hipLaunchKernelGGL((sel_attn_generic<uint16_t, Rows>), dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a,
+                       rows);
+  else
+    hipLaunchKernelGGL((sel_attn_generic<float, Rows>), dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a,
+                       rows);
+}
+
+bool chunks_tile_aligned(const Geo& g) {
+  for (int c = 0; c < g.N; ++c)
+    if (g.cs[c] % kKT) return false;
+  return true;
+}
+
+cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv, int lb, int le,
                            const int32_t* sel, int64_t n_sel, const void* qf, bool q_by_slot, void* out, float* lse,
                            void* ws, hipStream_t s) {
   const int layers = le - lb;
   if (p.mfma) {
+    if (cv.paged && !chunks_tile_aligned(g))
+      return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
     AttnArgs a;
     a.q = (const uint16_t*)qf;
-    a.k = (const uint16_t*)k;
-    a.v = (const uint16_t*)v;
     a.sel = sel;
     a.out = (uint16_t*)out;
     a.lse = lse;
@@ -937,22 +988,13 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const
     a.part_cap = p.part_cap;
     a.q_by_slot = q_by_slot ? 1 : 0;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g.D));
-    switch (g.G) {
-      case 1: launch_mfma_g<1>(a, s); break;
-      case 2: launch_mfma_g<2>(a, s); break;
-      case 4: launch_mfma_g<4>(a, s); break;
-      case 8: launch_mfma_g<8>(a, s); break;
-      case 16: launch_mfma_g<16>(a, s); break;
-      case 32: launch_mfma_g<32>(a, s); break;
-      default: return fail(CS_ERR_UNSUPPORTED, "MFMA attention needs H_q/H_kv dividing 32");
-    }
+    const cs_status st = cv.paged ? launch_mfma(g.G, a, cv.pages<kMaxPages>(g), s) : launch_mfma(g.G, a, cv.flat(g), s);
+    if (st) return st;
     return check_launch("selective attention launch");
   }
   GenAttnArgs a;
   a.q = qf;
   a.q_by_slot = q_by_slot ? 1 : 0;
-  a.k = k;
-  a.v = v;
   a.sel = sel;
   a.out = out;
   a.lse = lse;
@@ -966,11 +1008,8 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const void* k, const
   a.D = g.D;
   a.lb = lb;
   a.scale = (float)(1.0 / sqrt((double)g.D));
-  TraceScope tr("sel_attn_generic", s);
-  if (g.dtype == CS_BF16)
-    hipLaunchKernelGGL(sel_attn_generic<uint16_t>, dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a);
-  else
-    hipLaunchKernelGGL(sel_attn_generic<float>, dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a);
+  if (cv.paged) launch_generic(g, a, cv.pages<kMaxPages>(g), n_sel, layers, s);
+  else launch_generic(g, a, cv.flat(g), n_sel, layers, s);
   return check_launch("generic attention launch");
 }
 

@@ -107,14 +107,100 @@ __device__ __forceinline__ void rotate8(u32x4& wa, u32x4& wb, const float* c, co
   }
 }
 
+// ------------------------------------------------------------------ cache row addressing
+// A contiguous cache is one buffer per tensor, [L][H_kv][T][D].  A paged
+// cache keeps chunk c in buffers of its own, [L][H_kv][len_c][D] with
+// len_c = start[c+1] - start[c]: the chunks stay where they were loaded and
+// are never concatenated (Section 2 stores every chunk's cache on its own).
+// Kernels reach a row through one of these two maps, a template argument, so
+// the contiguous instantiation keeps its plain address arithmetic.
+// plane = layer * H_kv + KV head; t = composed token index.
+struct FlatRows {
+  char* k;
+  char* v;
+  int64_t T;
+  __device__ __forceinline__ char* row(bool val, int64_t plane, int64_t t, int row_bytes) const {
+    return (val ? v : k) + (plane * T + t) * row_bytes;
+  }
+  __device__ __forceinline__ void kv_rows(int64_t plane, int64_t t, int row_bytes, char*& kr, char*& vr) const {
+    const int64_t o = (plane * T + t) * row_bytes;
+    kr = k + o;
+    vr = v + o;
+  }
+};
+
+// Up to CAP chunks, carried in the kernel arguments.  The bf16 / D = 128
+// kernels take 128; kernels whose arguments also hold a 256-entry float64
+// table take 64, so that every argument block stays within 4 KB.
+template <int CAP>
+struct PagedRowsT {
+  static constexpr int kCap = CAP;
+  int n;               // chunks
+  int start[CAP + 1];  // token start of each chunk, start[n] = T
+  char* k[CAP];
+  char* v[CAP];        // NULL entries when only keys are addressed
+  // chunk of token t (0 <= t < T): the largest c with start[c] <= t
+  __device__ __forceinline__ int chunk_of(int64_t t) const {
+    int lo = 0, hi = n;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (start[mid] <= t) lo = mid;
+      else hi = mid;
+    }
+    return lo;
+  }
+  __device__ __forceinline__ char* row(bool val, int64_t plane, int64_t t, int row_bytes) const {
+    const int c = chunk_of(t);
+    const int64_t len = start[c + 1] - start[c];
+    return (val ? v[c] : k[c]) + (plane * len + (t - start[c])) * row_bytes;
+  }
+  __device__ __forceinline__ void kv_rows(int64_t plane, int64_t t, int row_bytes, char*& kr, char*& vr) const {
+    const int c = chunk_of(t);
+    const int64_t o = (plane * (int64_t)(start[c + 1] - start[c]) + (t - start[c])) * row_bytes;
+    kr = k[c] + o;
+    vr = v[c] + o;
+  }
+};
+constexpr int kMaxPages = 128;
+constexpr int kMaxPagesGeneric = 64;
+using PagedRows = PagedRowsT<kMaxPages>;
+using PagedRowsG = PagedRowsT<kMaxPagesGeneric>;
+
+// Host-side description of either layout, as the entry points receive it.
+struct CacheView {
+  bool paged = false;
+  void* k = nullptr;  // contiguous buffers
+  void* v = nullptr;
+  void* const* k_chunks = nullptr;  // paged: HOST [N] device pointers
+  void* const* v_chunks = nullptr;  // (NULL: keys only)
+  FlatRows flat(const Geo& g) const {
+    FlatRows r;
+    r.k = (char*)k;
+    r.v = (char*)v;
+    r.T = g.T;
+    return r;
+  }
+  template <int CAP>
+  PagedRowsT<CAP> pages(const Geo& g) const {  // caller checked g.N <= CAP
+    PagedRowsT<CAP> r;
+    r.n = g.N;
+    for (int c = 0; c <= g.N; ++c) r.start[c] = (int)g.cs[c];
+    for (int c = 0; c < g.N; ++c) {
+      r.k[c] = (char*)k_chunks[c];
+      r.v[c] = v_chunks ? (char*)v_chunks[c] : nullptr;
+    }
+    return r;
+  }
+};
+
 // ------------------------------------------------------------------ launches (per source file)
-cs_status launch_rebase(const Geo& g, void* k, const int32_t* offsets, const double* theta,
+cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* offsets, const double* theta,
                         hipStream_t s);
-cs_status launch_rebase_tokens(const Geo& g, void* k, const int32_t* token_offsets, const double* theta,
+cs_status launch_rebase_tokens(const Geo& g, const CacheView& cv, const int32_t* token_offsets, const double* theta,
                                hipStream_t s);
-cs_status launch_score_select(const Geo& g, const void* k_layer, const void* k_fresh, float* scores,
+cs_status launch_score_select(const Geo& g, const CacheView& cv, int score_layer, const void* k_fresh, float* scores,
                               int32_t* sel, int64_t k_sel, hipStream_t s);
-cs_status launch_scatter(const Geo& g, void* k, void* v, int lb, int le, const int32_t* sel,
+cs_status launch_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel,
                          int64_t n_sel, const void* kf, const void* vf, hipStream_t s);
 
 struct AttnPlan {
@@ -126,10 +212,12 @@ struct AttnPlan {
   size_t ws_bytes_per_layer;  // per layer in the call: partial segments
 };
 AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call);
-cs_status launch_attention(const Geo& g, const AttnPlan& plan, const void* k, const void* v,
+// Every chunk starts at a multiple of the 64-key tile (a paged cache on the MFMA path needs it).
+bool chunks_tile_aligned(const Geo& g);
+cs_status launch_attention(const Geo& g, const AttnPlan& plan, const CacheView& cv,
                            int lb, int le, const int32_t* sel, int64_t n_sel, const void* qf,
                            bool q_by_slot, void* out, float* lse, void* ws, hipStream_t s);
-cs_status launch_rope_scatter(const Geo& g, void* k, void* v, int lb, int le, const int32_t* sel, int64_t n_sel,
+cs_status launch_rope_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
                               const void* q_pre, const void* k_pre, const void* v_new, const int32_t* coords,
                               const double* theta, void* q_ws, hipStream_t s);
 

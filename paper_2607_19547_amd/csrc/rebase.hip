@@ -23,18 +23,21 @@ constexpr int kFastPG = 2;   // planes (layer x kv head) per workgroup
 constexpr int kFastR = (kFastPG * kFastTB) / 32;  // rows per lane group (256 threads = 32 lane groups)
 static_assert((kFastPG * kFastTB) % 32 == 0, "a workgroup covers whole lane-group steps");
 
+// Chunk q of a launch: its first row of plane 0 at base[q], planes
+// `plane_stride` rows apart (T for a contiguous cache, len[q] for a paged one).
 struct RebaseFastArgs {
-  uint16_t* k;
   int64_t T;
   int planes;
   int sec0, sec01;
   int tblocks;  // token blocks of the longest chunk in this launch
   int nc;       // chunks in this launch
+  int paged;
   double theta[64];
-  int start[kFastMaxChunks];
+  uint16_t* base[kFastMaxChunks];
   int len[kFastMaxChunks];
   int off[kFastMaxChunks][3];
 };
+static_assert(sizeof(RebaseFastArgs) <= 4096, "kernel arguments within 4 KB");
 
 
 // Lane layout: 8 lanes per 256-byte row; lane j of the row owns pairs
@@ -55,7 +58,7 @@ __global__ __launch_bounds__(256) void rebase_bf16_d128(const RebaseFastArgs a) 
   if (t0 >= len) return;  // whole workgroup
   const int j = threadIdx.x & 7;
   const int r0 = threadIdx.x >> 3;  // 0..31
-  const int64_t base_tok = a.start[c] + t0;
+  const int64_t pstride = a.paged ? len : a.T;
   u32x4 wa[kFastR], wb[kFastR];
   uint16_t* row[kFastR];
   bool ok[kFastR];
@@ -65,7 +68,7 @@ __global__ __launch_bounds__(256) void rebase_bf16_d128(const RebaseFastArgs a) 
     const int plane = pg * kFastPG + idx / kFastTB;
     const int tok = idx % kFastTB;
     ok[u] = plane < a.planes && t0 + tok < len;
-    row[u] = a.k + ((int64_t)plane * a.T + base_tok + tok) * 128;
+    row[u] = a.base[c] + ((int64_t)plane * pstride + t0 + tok) * 128;
     if (ok[u]) {
       wa[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 8 * j));
       wb[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 64 + 8 * j));
@@ -99,16 +102,17 @@ constexpr int kGenMaxChunks = 32;
 constexpr int kGenTB = 32;
 
 struct RebaseGenArgs {
-  void* k;
   int64_t T;
   int planes, D, P;
   int sec0, sec01;
   int tblocks;
+  int paged;
   double theta[256];
-  int start[kGenMaxChunks];
+  char* base[kGenMaxChunks];  // as in RebaseFastArgs
   int len[kGenMaxChunks];
   int off[kGenMaxChunks][3];
 };
+static_assert(sizeof(RebaseGenArgs) <= 4096, "kernel arguments within 4 KB");
 
 template <typename E>
 __device__ __forceinline__ float ld(const E* p);
@@ -137,11 +141,12 @@ __global__ __launch_bounds__(256) void rebase_generic(const RebaseGenArgs a) {
     tab[i] = cos_sin_of(phi);
   }
   __syncthreads();
-  E* k = (E*)a.k;
+  E* k = (E*)a.base[c];
+  const int64_t pstride = a.paged ? len : a.T;
   const int ntok = min(kGenTB, len - t0);
   for (int w = threadIdx.x; w < ntok * a.P; w += blockDim.x) {
     const int tok = w / a.P, i = w % a.P;
-    E* row = k + ((int64_t)plane * a.T + a.start[c] + t0 + tok) * a.D;
+    E* row = k + ((int64_t)plane * pstride + t0 + tok) * a.D;
     const float x = ld(row + i), y = ld(row + i + a.P);
     const float2 t = tab[i];
     st(row + i, fmaf(x, t.x, -y * t.y));
@@ -160,16 +165,17 @@ constexpr int kTokTB = 64;  // tokens per workgroup
 constexpr int kTokPG = 8;   // planes per workgroup
 constexpr int kTokTabW = 65;  // table row stride (float2): one pad entry spreads the LDS banks
 
+template <int P_MAX>
 struct RebaseTokArgs {
-  void* k;
   const int32_t* off;  // DEVICE [T][3]
   int64_t T;
   int planes, D, P;
   int sec0, sec01;
-  double theta[256];
+  double theta[P_MAX];
 };
 
-__global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokArgs a) {
+template <typename Rows>
+__global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokArgs<64> a, const Rows rows) {
   __shared__ float2 tab[kTokTB * kTokTabW];
   __shared__ int moved[kTokTB];
   const int64_t t0 = (int64_t)blockIdx.x * kTokTB;
@@ -193,7 +199,6 @@ __global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokAr
     moved[tok] = mv;
   }
   __syncthreads();
-  uint16_t* k = (uint16_t*)a.k;
   const int j = threadIdx.x & 7;
   const int r0 = threadIdx.x >> 3;  // 0..31
 #pragma unroll 1
@@ -208,8 +213,8 @@ __global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokAr
       const int plane = blockIdx.y * kTokPG + idx / kTokTB;
       tk[u] = idx % kTokTB;
       ok[u] = plane < a.planes && tk[u] < ntok && moved[tk[u]];
-      row[u] = k + ((int64_t)plane * a.T + t0 + tk[u]) * 128;
       if (ok[u]) {
+        row[u] = (uint16_t*)rows.row(false, plane, t0 + tk[u], 256);
         wa[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 8 * j));
         wb[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 64 + 8 * j));
       }
@@ -233,13 +238,13 @@ __global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokAr
 }
 
 // Any head_dim and either dtype: one workgroup per (token, plane), one pair per thread.
-template <typename E>
-__global__ __launch_bounds__(64) void rebase_tokens_generic(const RebaseTokArgs a) {
+template <typename E, typename Rows>
+__global__ __launch_bounds__(64) void rebase_tokens_generic(const RebaseTokArgs<256> a, const Rows rows) {
   const int64_t t = blockIdx.x;
   const int plane = blockIdx.y;
   const int32_t* o = a.off + t * 3;
   if ((o[0] | o[1] | o[2]) == 0) return;  // whole workgroup
-  E* row = (E*)a.k + ((int64_t)plane * a.T + t) * a.D;
+  E* row = (E*)rows.row(false, plane, t, a.D * (int)sizeof(E));
   for (int i = threadIdx.x; i < a.P; i += blockDim.x) {
     const float2 cs = cos_sin_of((double)o[axis_of(i, a.sec0, a.sec01)] * a.theta[i]);
     const float x = ld(row + i), y = ld(row + i + a.P);
@@ -248,9 +253,8 @@ __global__ __launch_bounds__(64) void rebase_tokens_generic(const RebaseTokArgs 
   }
 }
 
-cs_status launch_rebase_tokens(const Geo& g, void* k, const int32_t* off, const double* theta, hipStream_t s) {
-  RebaseTokArgs a;
-  a.k = k;
+template <int P_MAX>
+static void fill_tok_args(RebaseTokArgs<P_MAX>& a, const Geo& g, const int32_t* off, const double* theta) {
   a.off = off;
   a.T = g.T;
   a.planes = g.L * g.Hkv;
@@ -259,23 +263,45 @@ cs_status launch_rebase_tokens(const Geo& g, void* k, const int32_t* off, const 
   a.sec0 = g.sec[0];
   a.sec01 = g.sec[0] + g.sec[1];
   for (int i = 0; i < g.P; ++i) a.theta[i] = theta[i];
+}
+
+template <typename Rows>
+static void launch_tok_fast(const RebaseTokArgs<64>& a, const Rows& rows, hipStream_t s) {
+  static_assert(sizeof(RebaseTokArgs<64>) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
+  TraceScope tr("rebase_tokens_bf16_d128", s);
+  hipLaunchKernelGGL(rebase_tokens_bf16_d128<Rows>, dim3((unsigned)((a.T + kTokTB - 1) / kTokTB),
+                                                         (unsigned)((a.planes + kTokPG - 1) / kTokPG)),
+                     dim3(256), 0, s, a, rows);
+}
+
+template <typename Rows>
+static void launch_tok_generic(const Geo& g, const RebaseTokArgs<256>& a, const Rows& rows, hipStream_t s) {
+  static_assert(sizeof(RebaseTokArgs<256>) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
+  TraceScope tr("rebase_tokens_generic", s);
+  if (g.dtype == CS_BF16)
+    hipLaunchKernelGGL((rebase_tokens_generic<uint16_t, Rows>), dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a, rows);
+  else
+    hipLaunchKernelGGL((rebase_tokens_generic<float, Rows>), dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a, rows);
+}
+
+cs_status launch_rebase_tokens(const Geo& g, const CacheView& cv, const int32_t* off, const double* theta,
+                               hipStream_t s) {
   if (g.dtype == CS_BF16 && g.D == 128) {
-    TraceScope tr("rebase_tokens_bf16_d128", s);
-    hipLaunchKernelGGL(rebase_tokens_bf16_d128, dim3((unsigned)((g.T + kTokTB - 1) / kTokTB),
-                                                     (unsigned)((a.planes + kTokPG - 1) / kTokPG)),
-                       dim3(256), 0, s, a);
+    RebaseTokArgs<64> a;
+    fill_tok_args(a, g, off, theta);
+    if (cv.paged) launch_tok_fast(a, cv.pages<kMaxPages>(g), s);
+    else launch_tok_fast(a, cv.flat(g), s);
   } else {
-    TraceScope tr("rebase_tokens_generic", s);
-    if (g.dtype == CS_BF16)
-      hipLaunchKernelGGL(rebase_tokens_generic<uint16_t>, dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a);
-    else
-      hipLaunchKernelGGL(rebase_tokens_generic<float>, dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a);
+    RebaseTokArgs<256> a;
+    fill_tok_args(a, g, off, theta);
+    if (cv.paged) launch_tok_generic(g, a, cv.pages<kMaxPagesGeneric>(g), s);
+    else launch_tok_generic(g, a, cv.flat(g), s);
   }
   return check_launch("per-token rebase kernel launch");
 }
 
 // ---------------------------------------------------------------- host launcher
-cs_status launch_rebase(const Geo& g, void* k, const int32_t* off, const double* theta,
+cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, const double* theta,
                         hipStream_t s) {
   std::vector<int> todo;
   for (int c = 0; c < g.N; ++c)
@@ -283,6 +309,10 @@ cs_status launch_rebase(const Geo& g, void* k, const int32_t* off, const double*
   const int planes = g.L * g.Hkv;
   const bool fast = g.dtype == CS_BF16 && g.D == 128;
   const int per = fast ? kFastMaxChunks : kGenMaxChunks;
+  // first row of plane 0 of chunk c
+  auto chunk_base = [&](int c) -> char* {
+    return cv.paged ? (char*)cv.k_chunks[c] : (char*)cv.k + g.cs[c] * (int64_t)g.D * g.esize;
+  };
   for (size_t b = 0; b < todo.size(); b += per) {
     const int nc = (int)std::min<size_t>(per, todo.size() - b);
     int maxlen = 0;
@@ -292,26 +322,25 @@ cs_status launch_rebase(const Geo& g, void* k, const int32_t* off, const double*
     }
     if (fast) {
       RebaseFastArgs a;
-      a.k = (uint16_t*)k;
       a.T = g.T;
       a.planes = planes;
       a.sec0 = g.sec[0];
       a.sec01 = g.sec[0] + g.sec[1];
       a.tblocks = (maxlen + kFastTB - 1) / kFastTB;
+      a.nc = nc;
+      a.paged = cv.paged ? 1 : 0;
       for (int i = 0; i < 64; ++i) a.theta[i] = theta[i];
       for (int q = 0; q < nc; ++q) {
         const int c = todo[b + q];
-        a.start[q] = (int)g.cs[c];
+        a.base[q] = (uint16_t*)chunk_base(c);
         a.len[q] = (int)(g.cs[c + 1] - g.cs[c]);
         for (int x = 0; x < 3; ++x) a.off[q][x] = off[3 * c + x];
       }
       const int pgroups = (planes + kFastPG - 1) / kFastPG;
       TraceScope tr("rebase_bf16_d128", s);
-      a.nc = nc;
       hipLaunchKernelGGL(rebase_bf16_d128, dim3((unsigned)(a.tblocks * pgroups * nc)), dim3(256), 0, s, a);
     } else {
       RebaseGenArgs a;
-      a.k = k;
       a.T = g.T;
       a.planes = planes;
       a.D = g.D;
@@ -319,10 +348,11 @@ cs_status launch_rebase(const Geo& g, void* k, const int32_t* off, const double*
       a.sec0 = g.sec[0];
       a.sec01 = g.sec[0] + g.sec[1];
       a.tblocks = (maxlen + kGenTB - 1) / kGenTB;
+      a.paged = cv.paged ? 1 : 0;
       for (int i = 0; i < g.P; ++i) a.theta[i] = theta[i];
       for (int q = 0; q < nc; ++q) {
         const int c = todo[b + q];
-        a.start[q] = (int)g.cs[c];
+        a.base[q] = chunk_base(c);
         a.len[q] = (int)(g.cs[c + 1] - g.cs[c]);
         for (int x = 0; x < 3; ++x) a.off[q][x] = off[3 * c + x];
       }

@@ -23,8 +23,6 @@ constexpr int kRsTok = 8;       // selected tokens per workgroup
 constexpr int kRsTabW = 65;     // table row stride (float2): one pad entry spreads the LDS banks
 
 struct RopeScatterArgs {
-  uint16_t* k;            // cache [L][H_kv][T][128]
-  uint16_t* v;
   uint16_t* q_ws;         // [layers in call][H_q][n_sel][128]
   const uint16_t* q_pre;  // [L][H_q][n][128]
   const uint16_t* k_pre;  // [L][H_kv][n][128]
@@ -37,7 +35,9 @@ struct RopeScatterArgs {
   double theta[64];
 };
 
-__global__ __launch_bounds__(256) void rope_scatter_bf16_d128(const RopeScatterArgs a) {
+// Cache rows (K, V) are reached through the row map `rows`.
+template <typename Rows>
+__global__ __launch_bounds__(256) void rope_scatter_bf16_d128(const RopeScatterArgs a, const Rows rows) {
   __shared__ float2 tab[kRsTok * kRsTabW];
   __shared__ int tok_of[kRsTok];
   const int64_t m0 = (int64_t)blockIdx.x * kRsTok;
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(256) void rope_scatter_bf16_d128(const RopeScatterA
         const bool is_k = kind < a.Hkv;
         const int h = is_k ? kind : kind - a.Hkv;
         src = (is_k ? a.k_pre : a.v_new) + (((int64_t)layer * a.Hkv + h) * a.n + (t - a.cs1)) * 128;
-        dst[u] = (is_k ? a.k : a.v) + (((int64_t)layer * a.Hkv + h) * a.T + t) * 128;
+        dst[u] = (uint16_t*)rows.row(!is_k, (int64_t)layer * a.Hkv + h, t, 256);
       } else {
         const int h = kind - 2 * a.Hkv;
         src = a.q_pre + (((int64_t)layer * a.Hq + h) * a.n + (t - a.cs1)) * 128;
@@ -117,8 +117,6 @@ __global__ __launch_bounds__(256) void rope_scatter_bf16_d128(const RopeScatterA
 
 // Any head_dim and either dtype: one workgroup per (selected slot, layer).
 struct RopeScatterGenArgs {
-  void* k;
-  void* v;
   void* q_ws;
   const void* q_pre;
   const void* k_pre;
@@ -144,8 +142,8 @@ __device__ __forceinline__ void stx<float>(float* p, float x) { *p = x; }
 template <>
 __device__ __forceinline__ void stx<uint16_t>(uint16_t* p, float x) { *p = f32_to_bf16(x); }
 
-template <typename E>
-__global__ __launch_bounds__(64) void rope_scatter_generic(const RopeScatterGenArgs a) {
+template <typename E, typename Rows>
+__global__ __launch_bounds__(64) void rope_scatter_generic(const RopeScatterGenArgs a, const Rows rows) {
   const int64_t m = blockIdx.x;
   const int layer = a.lb + blockIdx.y;
   const int64_t t = a.sel[m];
@@ -155,12 +153,14 @@ __global__ __launch_bounds__(64) void rope_scatter_generic(const RopeScatterGenA
     const float2 cs = cos_sin_of((double)a.coords[t * 3 + axis_of(i, a.sec0, a.sec01)] * a.theta[i]);
     for (int h = 0; h < a.Hkv; ++h) {
       const E* kp = (const E*)a.k_pre + (((int64_t)layer * a.Hkv + h) * a.n + r) * a.D;
-      E* kd = (E*)a.k + (((int64_t)layer * a.Hkv + h) * a.T + t) * a.D;
+      char *kr, *vr;
+      rows.kv_rows((int64_t)layer * a.Hkv + h, t, a.D * (int)sizeof(E), kr, vr);
+      E* kd = (E*)kr;
       const float x = ldx(kp + i), y = ldx(kp + i + a.P);
       stx(kd + i, fmaf(x, cs.x, -y * cs.y));
       stx(kd + i + a.P, fmaf(x, cs.y, y * cs.x));
       const E* vp = (const E*)a.v_new + (((int64_t)layer * a.Hkv + h) * a.n + r) * a.D;
-      E* vd = (E*)a.v + (((int64_t)layer * a.Hkv + h) * a.T + t) * a.D;
+      E* vd = (E*)vr;
       vd[i] = vp[i];
       vd[i + a.P] = vp[i + a.P];
     }
@@ -174,13 +174,30 @@ __global__ __launch_bounds__(64) void rope_scatter_generic(const RopeScatterGenA
   }
 }
 
-cs_status launch_rope_scatter(const Geo& g, void* k, void* v, int lb, int le, const int32_t* sel, int64_t n_sel,
+template <typename Rows>
+static void launch_rs_fast(const RopeScatterArgs& a, const Rows& rows, int64_t n_sel, int layers, hipStream_t s) {
+  static_assert(sizeof(RopeScatterArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
+  TraceScope tr("rope_scatter_bf16_d128", s);
+  hipLaunchKernelGGL(rope_scatter_bf16_d128<Rows>, dim3((unsigned)((n_sel + kRsTok - 1) / kRsTok), layers),
+                     dim3(256), 0, s, a, rows);
+}
+
+template <typename Rows>
+static void launch_rs_generic(const Geo& g, const RopeScatterGenArgs& a, const Rows& rows, int64_t n_sel, int layers,
+                              hipStream_t s) {
+  static_assert(sizeof(RopeScatterGenArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
+  TraceScope tr("rope_scatter_generic", s);
+  if (g.dtype == CS_BF16)
+    hipLaunchKernelGGL((rope_scatter_generic<uint16_t, Rows>), dim3((unsigned)n_sel, layers), dim3(64), 0, s, a, rows);
+  else
+    hipLaunchKernelGGL((rope_scatter_generic<float, Rows>), dim3((unsigned)n_sel, layers), dim3(64), 0, s, a, rows);
+}
+
+cs_status launch_rope_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
                               const void* q_pre, const void* k_pre, const void* v_new, const int32_t* coords,
                               const double* theta, void* q_ws, hipStream_t s) {
   if (g.dtype == CS_BF16 && g.D == 128) {
     RopeScatterArgs a;
-    a.k = (uint16_t*)k;
-    a.v = (uint16_t*)v;
     a.q_ws = (uint16_t*)q_ws;
     a.q_pre = (const uint16_t*)q_pre;
     a.k_pre = (const uint16_t*)k_pre;
@@ -197,13 +214,10 @@ cs_status launch_rope_scatter(const Geo& g, void* k, void* v, int lb, int le, co
     a.sec0 = g.sec[0];
     a.sec01 = g.sec[0] + g.sec[1];
     for (int i = 0; i < 64; ++i) a.theta[i] = theta[i];
-    TraceScope tr("rope_scatter_bf16_d128", s);
-    hipLaunchKernelGGL(rope_scatter_bf16_d128, dim3((unsigned)((n_sel + kRsTok - 1) / kRsTok), le - lb), dim3(256),
-                       0, s, a);
+    if (cv.paged) launch_rs_fast(a, cv.pages<kMaxPages>(g), n_sel, le - lb, s);
+    else launch_rs_fast(a, cv.flat(g), n_sel, le - lb, s);
   } else {
     RopeScatterGenArgs a;
-    a.k = k;
-    a.v = v;
     a.q_ws = q_ws;
     a.q_pre = q_pre;
     a.k_pre = k_pre;
@@ -222,11 +236,8 @@ cs_status launch_rope_scatter(const Geo& g, void* k, void* v, int lb, int le, co
     a.sec0 = g.sec[0];
     a.sec01 = g.sec[0] + g.sec[1];
     for (int i = 0; i < g.P; ++i) a.theta[i] = theta[i];
-    TraceScope tr("rope_scatter_generic", s);
-    if (g.dtype == CS_BF16)
-      hipLaunchKernelGGL(rope_scatter_generic<uint16_t>, dim3((unsigned)n_sel, le - lb), dim3(64), 0, s, a);
-    else
-      hipLaunchKernelGGL(rope_scatter_generic<float>, dim3((unsigned)n_sel, le - lb), dim3(64), 0, s, a);
+    if (cv.paged) launch_rs_generic(g, a, cv.pages<kMaxPagesGeneric>(g), n_sel, le - lb, s);
+    else launch_rs_generic(g, a, cv.flat(g), n_sel, le - lb, s);
   }
   return check_launch("rope scatter launch");
 }

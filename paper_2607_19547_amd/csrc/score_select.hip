@@ -22,18 +22,18 @@ __device__ __forceinline__ double ldd<float>(const float* p) { return (double)*p
 template <>
 __device__ __forceinline__ double ldd<uint16_t>(const uint16_t* p) { return (double)bf16_to_f32(*p); }
 
-// One wavefront per candidate token.
-template <typename E>
-__global__ __launch_bounds__(256) void deviation_score(const E* __restrict__ k_layer,
-                                                       const E* __restrict__ kf,
-                                                       float* __restrict__ scores, int64_t T,
+// One wavefront per candidate token.  Rows of the score layer are reached
+// through the cache's row map (plane = score_layer * H_kv + head).
+template <typename E, typename Rows>
+__global__ __launch_bounds__(256) void deviation_score(const Rows rows, const E* __restrict__ kf,
+                                                       float* __restrict__ scores, int score_layer,
                                                        int64_t n, int64_t cs1, int Hkv, int D) {
   const int64_t tok = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (tok >= n) return;  // whole wavefront
   const int lane = threadIdx.x & 63;
   double acc = 0.0;
   for (int h = 0; h < Hkv; ++h) {
-    const E* a = k_layer + ((int64_t)h * T + cs1 + tok) * D;
+    const E* a = (const E*)rows.row(false, (int64_t)score_layer * Hkv + h, cs1 + tok, D * (int)sizeof(E));
     const E* b = kf + ((int64_t)h * n + tok) * D;
     for (int d = lane; d < D; d += 64) {
       const double x = ldd(b + d) - ldd(a + d);
@@ -46,16 +46,16 @@ __global__ __launch_bounds__(256) void deviation_score(const E* __restrict__ k_l
 }
 
 // bf16, D = 128: 16 lanes per token, 8 elements per lane per head.
-__global__ __launch_bounds__(256) void deviation_score_bf16_d128(const uint16_t* __restrict__ k_layer,
-                                                                 const uint16_t* __restrict__ kf,
-                                                                 float* __restrict__ scores, int64_t T,
+template <typename Rows>
+__global__ __launch_bounds__(256) void deviation_score_bf16_d128(const Rows rows, const uint16_t* __restrict__ kf,
+                                                                 float* __restrict__ scores, int score_layer,
                                                                  int64_t n, int64_t cs1, int Hkv) {
   const int64_t tok = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
   const int j = threadIdx.x & 15;
   double acc = 0.0;
   if (tok < n) {
     for (int h = 0; h < Hkv; ++h) {
-      const u32x4 a = *(const u32x4*)(k_layer + ((int64_t)h * T + cs1 + tok) * 128 + 8 * j);
+      const u32x4 a = *(const u32x4*)((const uint16_t*)rows.row(false, (int64_t)score_layer * Hkv + h, cs1 + tok, 256) + 8 * j);
       const u32x4 b = *(const u32x4*)(kf + ((int64_t)h * n + tok) * 128 + 8 * j);
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
@@ -153,27 +153,30 @@ __global__ __launch_bounds__(kSelThreads) void radix_select_topk(const float* __
   }
 }
 
-cs_status launch_score_select(const Geo& g, const void* k_layer, const void* k_fresh, float* scores,
-                              int32_t* sel, int64_t k_sel, hipStream_t s) {
-  {
-    TraceScope tr("deviation_score", s);
-    if (g.dtype == CS_BF16 && g.D == 128) {
-      const int64_t blocks = (g.n + 15) / 16;
-      hipLaunchKernelGGL(deviation_score_bf16_d128, dim3((unsigned)blocks), dim3(256), 0, s,
-                         (const uint16_t*)k_layer, (const uint16_t*)k_fresh, scores, g.T, g.n, g.cs1,
-                         g.Hkv);
-    } else {
-      const int64_t blocks = (g.n + 3) / 4;
-      if (g.dtype == CS_BF16)
-        hipLaunchKernelGGL(deviation_score<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, s,
-                           (const uint16_t*)k_layer, (const uint16_t*)k_fresh, scores, g.T, g.n, g.cs1,
-                           g.Hkv, g.D);
-      else
-        hipLaunchKernelGGL(deviation_score<float>, dim3((unsigned)blocks), dim3(256), 0, s,
-                           (const float*)k_layer, (const float*)k_fresh, scores, g.T, g.n, g.cs1, g.Hkv,
-                           g.D);
-    }
+template <typename Rows>
+static void launch_score(const Geo& g, const Rows& rows, int score_layer, const void* k_fresh, float* scores,
+                         hipStream_t s) {
+  static_assert(sizeof(Rows) + 64 <= 4096, "kernel arguments within 4 KB");
+  TraceScope tr("deviation_score", s);
+  if (g.dtype == CS_BF16 && g.D == 128) {
+    const int64_t blocks = (g.n + 15) / 16;
+    hipLaunchKernelGGL(deviation_score_bf16_d128<Rows>, dim3((unsigned)blocks), dim3(256), 0, s, rows,
+                       (const uint16_t*)k_fresh, scores, score_layer, g.n, g.cs1, g.Hkv);
+  } else {
+    const int64_t blocks = (g.n + 3) / 4;
+    if (g.dtype == CS_BF16)
+      hipLaunchKernelGGL((deviation_score<uint16_t, Rows>), dim3((unsigned)blocks), dim3(256), 0, s, rows,
+                         (const uint16_t*)k_fresh, scores, score_layer, g.n, g.cs1, g.Hkv, g.D);
+    else
+      hipLaunchKernelGGL((deviation_score<float, Rows>), dim3((unsigned)blocks), dim3(256), 0, s, rows,
+                         (const float*)k_fresh, scores, score_layer, g.n, g.cs1, g.Hkv, g.D);
   }
+}
+
+cs_status launch_score_select(const Geo& g, const CacheView& cv, int score_layer, const void* k_fresh, float* scores,
+                              int32_t* sel, int64_t k_sel, hipStream_t s) {
+  if (cv.paged) launch_score(g, cv.pages<kMaxPages>(g), score_layer, k_fresh, scores, s);
+  else launch_score(g, cv.flat(g), score_layer, k_fresh, scores, s);
   cs_status st = check_launch("deviation score launch");
   if (st || k_sel == 0) return st;
   {

@@ -161,3 +161,40 @@ def test_fused_rope_argument_errors_and_workspace(built_lib):
     assert (b.selective_attend_scatter_rope_workspace(q, 6349, 1)
             >= b.selective_attend_scatter_workspace(q, 6349, 1) + 16 * 6349 * 128 * 2)
     b.selective_attend_scatter_rope(g, None, None, 0, 1, None, 0, None, None, None, None, None, stream=0)  # nothing to do
+
+
+def test_paged_argument_errors(built_lib):
+    g = _geo()
+    chunks = [FAKE, FAKE]
+    assert _code(b.compose_rebase_k_paged, g, None, np.zeros((2, 3)), stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    code, text = _code(b.compose_rebase_k_paged, g, [FAKE, None], np.zeros((2, 3)), stream=0)
+    assert code == b.CS_ERR_INVALID_ARGUMENT and "chunk 1" in text
+    assert _code(b.compose_rebase_k_tokens_paged, g, chunks, None, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    assert _code(b.score_deviation_topk_paged, g, chunks, 0, FAKE, 1.5, FAKE, FAKE,
+                 stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    # values are required by the attention calls
+    assert _code(b.selective_attend_scatter_paged, g, chunks, None, 0, 1, FAKE, 4, FAKE, FAKE, FAKE, FAKE,
+                 stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    assert _code(b.selective_attend_scatter_rope_paged, g, chunks, [FAKE, None], 0, 1, FAKE, 4, FAKE, FAKE, FAKE,
+                 FAKE, FAKE, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    # nothing to do: OK without looking at the chunk arrays
+    b.selective_attend_scatter_paged(g, None, None, 0, 1, None, 0, None, None, None, None, stream=0)
+
+
+def test_paged_limits(built_lib):
+    # more chunks than the chunk table holds
+    many = _geo(chunk_start=np.arange(66) * 2)            # 65 chunks, float32 / D = 16: at most 64
+    code, text = _code(b.compose_rebase_k_paged, many, [FAKE] * 65, np.zeros((65, 3)), stream=0)
+    assert code == b.CS_ERR_UNSUPPORTED and "64" in text
+    q = b.Geo(1, 16, 2, 128, (16, 24, 24), "bf16", np.arange(130) * 64)   # 129 chunks: at most 128
+    code, text = _code(b.score_deviation_topk_paged, q, [FAKE] * 129, 0, FAKE, 0.5, FAKE, FAKE, stream=0)
+    assert code == b.CS_ERR_UNSUPPORTED and "128" in text
+    # the MFMA attention reads whole 64-key tiles from one chunk
+    q = b.Geo(1, 16, 2, 128, (16, 24, 24), "bf16", [0, 100, 200])
+    assert b.selective_attend_scatter_workspace(q, 4, 1) <= FAKE.numel()
+    code, text = _code(b.selective_attend_scatter_paged, q, [FAKE] * 2, [FAKE] * 2, 0, 1, FAKE, 4, FAKE, FAKE, FAKE,
+                       FAKE, workspace=FAKE, stream=0)
+    assert code == b.CS_ERR_UNSUPPORTED and "64" in text
+    code, _ = _code(b.selective_attend_scatter_rope_paged, q, [FAKE] * 2, [FAKE] * 2, 0, 1, FAKE, 4, FAKE, FAKE, FAKE,
+                    FAKE, FAKE, workspace=FAKE, stream=0)
+    assert code == b.CS_ERR_UNSUPPORTED
