@@ -23,8 +23,8 @@ constexpr int kFastPG = 2;   // planes (layer x kv head) per workgroup
 constexpr int kFastR = (kFastPG * kFastTB) / 32;  // rows per lane group (256 threads = 32 lane groups)
 static_assert((kFastPG * kFastTB) % 32 == 0, "a workgroup covers whole lane-group steps");
 
-// Chunk q of a launch: its first row of plane 0 at base[q], planes
-// `plane_stride` rows apart (T for a contiguous cache, len[q] for a paged one).
+// Chunk q of a launch: its row of plane 0, token 0 at base[q]; planes are T
+// rows apart in a contiguous cache and len[q] rows apart in a chunk buffer.
 struct RebaseFastArgs {
   int64_t T;
   int planes;
@@ -42,38 +42,55 @@ static_assert(sizeof(RebaseFastArgs) <= 4096, "kernel arguments within 4 KB");
 
 // Lane layout: 8 lanes per 256-byte row; lane j of the row owns pairs
 // 8j..8j+7, i.e. 16 bytes in each half of the row.  A workgroup of 256
-// threads covers kFastPG planes x kFastTB tokens of one chunk, one row per
-// lane group and plane-token step, all loads issued (non-temporal: every byte
-// is touched once) before the chunk's table is built, then rotated and
-// stored.  Small workgroups in address order (token block fastest, then
-// chunk, then plane group) keep many independent streams in flight over
-// neighbouring memory.
+// threads covers kRows rows of one chunk, one row per lane group and step,
+// all loads issued (non-temporal: every byte is touched once) before the
+// chunk's table is built, then rotated and stored.  Small workgroups in
+// address order keep many independent streams in flight over neighbouring
+// memory.  Contiguous cache ([plane][T] rows): a workgroup takes kFastPG
+// planes x kFastTB tokens, token block fastest, then chunk, then plane group.
+// Paged cache: a chunk buffer is planes x len rows that all turn by the
+// chunk's table, so workgroups take runs of kRows consecutive rows, one
+// linear stream per chunk.
 __global__ __launch_bounds__(256) void rebase_bf16_d128(const RebaseFastArgs a) {
+  constexpr int kRows = kFastPG * kFastTB;
   __shared__ float2 tab[64];
   const int tb = blockIdx.x % a.tblocks;
-  const int c = (blockIdx.x / a.tblocks) % a.nc;
-  const int pg = blockIdx.x / (a.tblocks * a.nc);
+  const int rest = blockIdx.x / a.tblocks;
+  const int c = a.paged ? rest : rest % a.nc;
+  const int pg = rest / a.nc;  // (contiguous only)
   const int len = a.len[c];
-  const int t0 = tb * kFastTB;
-  if (t0 >= len) return;  // whole workgroup
   const int j = threadIdx.x & 7;
   const int r0 = threadIdx.x >> 3;  // 0..31
-  const int64_t pstride = a.paged ? len : a.T;
   u32x4 wa[kFastR], wb[kFastR];
   uint16_t* row[kFastR];
   bool ok[kFastR];
+  if (a.paged) {
+    const int64_t first = (int64_t)tb * kRows, rows = (int64_t)a.planes * len;
+    if (first >= rows) return;  // whole workgroup
 #pragma unroll
-  for (int u = 0; u < kFastR; ++u) {
-    const int idx = u * 32 + r0;
-    const int plane = pg * kFastPG + idx / kFastTB;
-    const int tok = idx % kFastTB;
-    ok[u] = plane < a.planes && t0 + tok < len;
-    row[u] = a.base[c] + ((int64_t)plane * pstride + t0 + tok) * 128;
+    for (int u = 0; u < kFastR; ++u) {
+      const int64_t r = first + u * 32 + r0;
+      ok[u] = r < rows;
+      row[u] = a.base[c] + r * 128;
+    }
+  } else {
+    const int t0 = tb * kFastTB;
+    if (t0 >= len) return;  // whole workgroup
+#pragma unroll
+    for (int u = 0; u < kFastR; ++u) {
+      const int idx = u * 32 + r0;
+      const int plane = pg * kFastPG + idx / kFastTB;
+      const int tok = idx % kFastTB;
+      ok[u] = plane < a.planes && t0 + tok < len;
+      row[u] = a.base[c] + ((int64_t)plane * a.T + t0 + tok) * 128;
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kFastR; ++u)
     if (ok[u]) {
       wa[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 8 * j));
       wb[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 64 + 8 * j));
     }
-  }
   if (threadIdx.x < 64) {
     const int i = threadIdx.x;
     const double phi = (double)a.off[c][axis_of(i, a.sec0, a.sec01)] * a.theta[i];
@@ -326,7 +343,9 @@ cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, c
       a.planes = planes;
       a.sec0 = g.sec[0];
       a.sec01 = g.sec[0] + g.sec[1];
-      a.tblocks = (maxlen + kFastTB - 1) / kFastTB;
+      // contiguous: token blocks of the longest chunk; paged: row runs of the largest chunk buffer
+      a.tblocks = cv.paged ? (int)(((int64_t)planes * maxlen + kFastPG * kFastTB - 1) / (kFastPG * kFastTB))
+                           : (maxlen + kFastTB - 1) / kFastTB;
       a.nc = nc;
       a.paged = cv.paged ? 1 : 0;
       for (int i = 0; i < 64; ++i) a.theta[i] = theta[i];
@@ -336,9 +355,9 @@ cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, c
         a.len[q] = (int)(g.cs[c + 1] - g.cs[c]);
         for (int x = 0; x < 3; ++x) a.off[q][x] = off[3 * c + x];
       }
-      const int pgroups = (planes + kFastPG - 1) / kFastPG;
+      const int pgroups = cv.paged ? 1 : (planes + kFastPG - 1) / kFastPG;
       TraceScope tr("rebase_bf16_d128", s);
-      hipLaunchKernelGGL(rebase_bf16_d128, dim3((unsigned)(a.tblocks * pgroups * nc)), dim3(256), 0, s, a);
+      hipLaunchKernelGGL(rebase_bf16_d128, dim3((unsigned)((int64_t)a.tblocks * pgroups * nc)), dim3(256), 0, s, a);
     } else {
       RebaseGenArgs a;
       a.T = g.T;
