@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--fused-rope-steps", type=int, default=3,
                    help="steps also timed through selective_attend_scatter_rope (pre-rotary fresh rows, "
                         "rotated at the global coordinates; 0: skip)")
+    p.add_argument("--gemm-context", type=int, default=1,
+                   help="also time the vendor library's bf16 GEMM on this GPU, as context for the MFMA figure (0: skip)")
     p.add_argument("--paged-steps", type=int, default=3,
                    help="steps also timed on the cache held as one buffer per chunk (0: skip)")
     p.add_argument("--batched-steps", type=int, default=3,
@@ -167,8 +169,32 @@ def main():
     paged = None
     if args.paged_steps > 0:
         paged = bench_rho(inp, w, rho, args.paged_steps, 1, binding, torch, False, paged=True)
+    gemm = gemm_context(torch) if args.gemm_context else None
     cpu = cpu_baseline(w, rho) if args.cpu_baseline else None
-    emit(args, w, rho, result, rho1, cpu, other, fused, paged)
+    emit(args, w, rho, result, rho1, cpu, other, fused, paged, gemm)
+
+
+def gemm_context(torch, m=8192, n=8192, k=16384, reps=10):
+    """bf16 GEMM rate of the vendor BLAS (torch.matmul -> hipBLASLt) on the same GPU and run: the dense
+    MFMA rate a tuned library reaches under the same clock and power limits (context only; the
+    roofline peak stays the published one)."""
+    a = torch.randn(m, k, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(k, n, device="cuda", dtype=torch.bfloat16)
+    for _ in range(3):
+        c = a @ b
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        c = a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    tf = 2.0 * m * n * k / (ms / 1e3) / 1e12
+    log(f"[bench] vendor bf16 GEMM {m}x{n}x{k}: {ms:.3f} ms, {tf:.1f} TFLOP/s")
+    del a, b, c
+    return dict(shape=[m, n, k], ms=round(ms, 4), TFLOPs=round(tf, 1))
 
 
 def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, paged=False):
@@ -423,7 +449,7 @@ def _traffic(kernel):
         return None
 
 
-def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None):
+def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=None):
     tr = r["trace"]
     steps = r["steps"]
     attn_n, attn_ms = tr.get("sel_attn_mfma", (0, 0.0))
@@ -497,6 +523,9 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None):
     if rho1 is not None:
         line["rho1_compose_ms"] = round(rho1["ms"], 3)
         line["rho1_over_rho_speedup"] = round(rho1["ms"] / r["ms"], 3)
+    if gemm is not None:
+        line["context_vendor_gemm_bf16"] = dict(gemm, sel_attn_over_gemm=None if attn_tflops is None
+                                                 else round(attn_tflops / gemm["TFLOPs"], 4))
     if cpu is not None:
         line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
