@@ -342,7 +342,30 @@ def sweep_rebase(args, b, synth, torch):
                      "flush": flush, "ms": round(med, 4), "ms_min": round(best, 4), "GBps": round(gbps, 1),
                      "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
         log(f"[bench] long65k scalar per-token flush={flush}: {med * 1e3:.1f} us, {gbps:.1f} GB/s")
+    # the same cache held as one buffer per chunk (the paged calls), per-chunk and per-token offsets
+    cs = w.chunk_start
+    Kc0 = [K0[:, :, cs[c]:cs[c + 1]].clone() for c in range(w.n_chunks)]
+    Kc = [x.clone() for x in Kc0]
     del K0, K
+    off = synth.chunk_offsets(w)
+    rot = int(sum(cs[c + 1] - cs[c] for c in range(w.n_chunks) if np.any(off[c])))
+    for label, fn, nb in (
+            ("long65k paged, per-chunk offsets", lambda: b.compose_rebase_k_paged(geo, Kc, off),
+             2 * w.n_layers * w.n_kv_heads * rot * w.head_dim * 2),
+            ("long65k paged, per-token scalar offsets", lambda: b.compose_rebase_k_tokens_paged(geo, Kc, toff),
+             nbytes)):
+        for flush in (True, False):
+            def before(flush=flush):
+                for x, x0 in zip(Kc, Kc0):
+                    x.copy_(x0)
+                if flush:
+                    junk.fill_(7)
+            med, best = _events(torch, stream, fn, args.steps + 1, before)
+            gbps = nb / (med * 1e-3) / 1e9
+            rows.append({"workload": label, "tokens": w.n_tokens, "bytes": nb, "flush": flush, "ms": round(med, 4),
+                         "ms_min": round(best, 4), "GBps": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
+            log(f"[bench] {label} flush={flush}: {med * 1e3:.1f} us, {gbps:.1f} GB/s")
+    del Kc, Kc0
     print(json.dumps({"metric": "rebase GB/s (% HBM peak) by cache size", "unit": "GB/s", "n_gpus": 1,
                       "higher_is_better": True, "dtype": "bf16", "data": "synthetic", "sweep": rows}), flush=True)
 

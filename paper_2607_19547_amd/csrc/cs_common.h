@@ -127,6 +127,11 @@ struct FlatRows {
     kr = k + o;
     vr = v + o;
   }
+  // Key row of token t in plane 0 and the byte distance between planes.
+  __device__ __forceinline__ void token_rows(int64_t t, int row_bytes, char*& k0, int64_t& plane_bytes) const {
+    k0 = k + t * row_bytes;
+    plane_bytes = T * row_bytes;
+  }
 };
 
 // Up to CAP chunks, carried in the kernel arguments.  The bf16 / D = 128
@@ -159,6 +164,11 @@ struct PagedRowsT {
     const int64_t o = (plane * (int64_t)(start[c + 1] - start[c]) + (t - start[c])) * row_bytes;
     kr = k[c] + o;
     vr = v[c] + o;
+  }
+  __device__ __forceinline__ void token_rows(int64_t t, int row_bytes, char*& k0, int64_t& plane_bytes) const {
+    const int c = chunk_of(t);
+    k0 = k[c] + (t - start[c]) * row_bytes;
+    plane_bytes = (int64_t)(start[c + 1] - start[c]) * row_bytes;
   }
 };
 constexpr int kMaxPages = 128;

@@ -195,6 +195,8 @@ template <typename Rows>
 __global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokArgs<64> a, const Rows rows) {
   __shared__ float2 tab[kTokTB * kTokTabW];
   __shared__ int moved[kTokTB];
+  __shared__ char* row0[kTokTB];         // the token's row in plane 0
+  __shared__ int64_t plane_bytes[kTokTB];  // and the distance between planes (one chunk lookup per token)
   const int64_t t0 = (int64_t)blockIdx.x * kTokTB;
   const int ntok = (int)min((int64_t)kTokTB, a.T - t0);
   for (int e = threadIdx.x; e < kTokTB * 64; e += 256) {
@@ -214,6 +216,7 @@ __global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokAr
       mv = (o[0] | o[1] | o[2]) != 0;
     }
     moved[tok] = mv;
+    if (tok < ntok) rows.token_rows(t0 + tok, 256, row0[tok], plane_bytes[tok]);
   }
   __syncthreads();
   const int j = threadIdx.x & 7;
@@ -231,7 +234,7 @@ __global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokAr
       tk[u] = idx % kTokTB;
       ok[u] = plane < a.planes && tk[u] < ntok && moved[tk[u]];
       if (ok[u]) {
-        row[u] = (uint16_t*)rows.row(false, plane, t0 + tk[u], 256);
+        row[u] = (uint16_t*)(row0[tk[u]] + plane * plane_bytes[tk[u]]);
         wa[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 8 * j));
         wb[u] = __builtin_nontemporal_load((const u32x4*)(row[u] + 64 + 8 * j));
       }
