@@ -681,29 +681,46 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
   __builtin_amdgcn_s_barrier();                     // and every wavefront is done with the ring
 
   const float l_tot = pair_sum(l_run);
+  // The wavefront's 32 result rows (query vector q, 256 bytes each) pass
+  // through its own 8 KB of the now idle V ring, so that every global store
+  // writes four whole rows instead of 16-byte pieces of 32 rows.  In LDS,
+  // 16-byte chunk c of row q sits at position c ^ (q & 15) (conflict-free
+  // writes of the accumulator layout).
+  char* tb = (wave < 2 ? lo_v0 : wave < 4 ? lo_v1 : wave < 6 ? lo_v2 : lo_v3) + (wave & 1) * (32 * kRow);
+  auto put = [&](int c, u32x2 w) {  // chunk c = elements 8c..8c+7 of row q; this lane holds half hi
+    *(u32x2*)(tb + q * kRow + ((c ^ (q & 15)) << 4) + 8 * hi) = w;
+  };
+  auto get = [&](int row, int c) -> u32x4 { return *(const u32x4*)(tb + row * kRow + ((c ^ (row & 15)) << 4)); };
   // accumulator register r of d-block b holds dim 32b + 8(r/4) + 4hi + r%4
   if (full) {
-    if (valid) {
-      const float inv = 1.f / l_tot;
-      uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128;
+    const float inv = valid ? 1.f / l_tot : 0.f;
 #pragma unroll
-      for (int d = 0; d < 4; ++d)
+    for (int d = 0; d < 4; ++d)
 #pragma unroll
-        for (int rq = 0; rq < 4; ++rq) {
-          u32x2 w;
-          w[0] = pack_bf16x2(o[d][4 * rq] * inv, o[d][4 * rq + 1] * inv);
-          w[1] = pack_bf16x2(o[d][4 * rq + 2] * inv, o[d][4 * rq + 3] * inv);
-          *(u32x2*)(op + 32 * d + 8 * rq + 4 * hi) = w;
-        }
-      if (a.lse && hi == 0)
-        a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (m_use + __log2f(l_tot)) * kLn2;
+      for (int rq = 0; rq < 4; ++rq) {
+        u32x2 w;
+        w[0] = pack_bf16x2(o[d][4 * rq] * inv, o[d][4 * rq + 1] * inv);
+        w[1] = pack_bf16x2(o[d][4 * rq + 2] * inv, o[d][4 * rq + 3] * inv);
+        put(4 * d + rq, w);
+      }
+    if (valid && a.lse && hi == 0)
+      a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (m_use + __log2f(l_tot)) * kLn2;
+    const uint64_t has_row = __ballot(valid);  // bit q: query vector q has an output row
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    // store s covers rows R = 4s .. 4s+3 in output order: head hh = R / RW, selected row j = R % RW
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const int R = 4 * s + (lane >> 4), c = lane & 15;
+      const int hh = R / RW, j = R % RW, qq = j * G + hh;
+      const u32x4 v = get(qq, c);
+      if ((has_row >> qq) & 1)
+        *(u32x4*)(a.out + (((int64_t)layer * a.Hq + kv * G + hh) * a.n_sel + m0 + wave * RW + j) * 128 + 8 * c) = v;
     }
   } else {
     // The piece's output row O / sum, scaled by 2^-e so that its largest
     // magnitude lies in [0.5, 1), is kept in fp16 (11 significant bits,
     // finer than the bf16 result; the scale keeps the bf16 range of V within
     // fp16's).
-    const int ql = wave * 32 + q;
     const int64_t slot = (int64_t)lrel * a.part_cap + pv.ppre[oi] + kv * nsp + piece;  // < part_cap per layer
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     float amax = 0.f;
@@ -714,20 +731,25 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     amax = pair_max(amax) * inv;
     const int e = amax > 0.f ? min(max(__builtin_amdgcn_frexp_expf(amax), -100), 100) : 0;  // 2^-e stays normal
     const float sc_e = inv * __builtin_ldexpf(1.f, -e);
-    uint16_t* pp = a.part + (slot * kQPerWG + ql) * 128;
 #pragma unroll
     for (int d = 0; d < 4; ++d)
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
         const f32x4 v4 = {o[d][4 * rq] * sc_e, o[d][4 * rq + 1] * sc_e, o[d][4 * rq + 2] * sc_e, o[d][4 * rq + 3] * sc_e};
-        *(f16x4*)(pp + 32 * d + 8 * rq + 4 * hi) = __builtin_convertvector(v4, f16x4);
+        put(4 * d + rq, __builtin_bit_cast(u32x2, __builtin_convertvector(v4, f16x4)));
       }
     if (hi == 0) {
       const f32x4 ml = {m_use, l_tot, (float)e, 0.f};
-      *(f32x4*)(a.part_ml + (slot * kQPerWG + ql) * 4) = ml;
+      *(f32x4*)(a.part_ml + (slot * kQPerWG + wave * 32 + q) * 4) = ml;
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    uint16_t* pp = a.part + (slot * kQPerWG + wave * 32) * 128;  // the wavefront's 32 consecutive rows
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const int R = 4 * s + (lane >> 4), c = lane & 15;
+      *(u32x4*)(pp + R * 128 + 8 * c) = get(R, c);
     }
   }
-
 }
 
 // Merge the pieces of every cut row tile, in piece order: one block per
