@@ -186,11 +186,16 @@ def test_paged_128_chunks():
         assert np.array_equal(flat[key], paged[key]), key
 
 
-def test_paged_rebase_tokens_and_fused_rope():
+@pytest.mark.parametrize("lens,G,Hkv,kind", [
+    ((256, 320, 192, 440), 8, 2, "bf16"),        # bf16 / D = 128 kernels
+    ((100, 130, 103, 167), 4, 2, "bf16-d32"),    # generic kernels, bf16
+    ((32, 32), 2, 2, "f32"),                     # generic kernels, float32
+])
+def test_paged_rebase_tokens_and_fused_rope(lens, G, Hkv, kind):
     """The per-token re-basing and the fused-rotary scatter on a paged cache
     give the contiguous calls' bits."""
-    w = workload((256, 320, 192, 440), G=8, Hkv=2)
-    log("case paged per-token rebase + fused rope")
+    w = _w(lens, G, Hkv, kind)
+    log(f"case paged per-token rebase + fused rope {kind}")
     d = oracle.inputs.build(w)
     b = B()
     geo = b.Geo.from_workload(w)
@@ -208,7 +213,8 @@ def test_paged_rebase_tokens_and_fused_rope():
     g_, o_ = dec(joined(Kp, dt), dt), dec(want, dt)
     assert np.all(np.abs(g_ - o_) <= ulp(o_, dt) + 2.0 ** -20 * pair_norm(o_))
     # fused rotary scatter + attention
-    sel = np.sort(np.random.default_rng(5).choice(np.arange(w.cs1, w.n_tokens), size=97, replace=False))
+    sel = np.sort(np.random.default_rng(5).choice(np.arange(w.cs1, w.n_tokens), size=min(97, w.n_candidates // 2),
+                                                  replace=False))
     S = torch.from_numpy(sel.astype(np.int32)).cuda()
     C = torch.from_numpy(np.ascontiguousarray(d["global_coords"], dtype=np.int32)).cuda()
     Q, KF, VF = to_dev(d["q_fresh"], dt), to_dev(d["k_fresh"], dt), to_dev(d["v_fresh"], dt)
