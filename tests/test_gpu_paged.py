@@ -235,3 +235,38 @@ def test_paged_rebase_tokens_and_fused_rope(lens, G, Hkv, kind):
                        to_host(out, dt), lse.cpu().numpy())
     for a, c in zip(outs[False], outs[True]):
         assert np.array_equal(a, c)
+
+
+def test_paged_long65k_equals_contiguous():
+    """The timed cache geometry (65,536 tokens in 32 chunk buffers of 2048) at rho = 0.1, first
+    two layers: the paged composition gives the contiguous one's bits in every output."""
+    import bench
+    w = dataclasses.replace(synth.WORKLOADS["long65k"], n_layers=2)
+    log("case paged long65k, two layers")
+    b = B()
+    inp = bench.Inputs(w, torch, b, synth)
+    cs, n = w.chunk_start, w.n_candidates
+    res = []
+    for paged in (False, True):
+        K, V = inp.K0.clone(), inp.V0.clone()
+        if paged:
+            K, V = split(K, cs), split(V, cs)
+            b.compose_rebase_k_paged(inp.geo, K, inp.offsets)
+        else:
+            b.compose_rebase_k(inp.geo, K, inp.offsets)
+        scores = torch.empty(n, dtype=torch.float32, device="cuda")
+        sel = torch.empty(n, dtype=torch.int32, device="cuda")
+        score = b.score_deviation_topk_paged if paged else b.score_deviation_topk
+        k = score(inp.geo, K, w.score_layer, inp.KF[w.score_layer], 0.1, scores, sel)
+        out = torch.empty((w.n_layers, w.n_q_heads, k, w.head_dim), dtype=torch.bfloat16, device="cuda")
+        lse = torch.empty((w.n_layers, w.n_q_heads, k), dtype=torch.float32, device="cuda")
+        ws = torch.empty(b.selective_attend_scatter_workspace(inp.geo, k, 1), dtype=torch.uint8, device="cuda")
+        attend = b.selective_attend_scatter_paged if paged else b.selective_attend_scatter
+        for layer in range(w.n_layers):
+            attend(inp.geo, K, V, layer, layer + 1, sel, k, inp.QF, inp.KF, inp.VF, out, lse, ws)
+        torch.cuda.synchronize()
+        Kh = torch.cat(K, dim=2) if paged else K
+        Vh = torch.cat(V, dim=2) if paged else V
+        res.append([scores.cpu(), sel[:k].cpu(), Kh.cpu(), Vh.cpu(), out.cpu(), lse.cpu()])
+    for x, y in zip(*res):
+        assert torch.equal(x, y)

@@ -463,6 +463,44 @@ def test_long65k_per_layer_sampled():
     _isolated_full_size(w, rhos=(0.1, 1.0), n_random=48, check_rebase=True)
 
 
+def test_attn32k_sampled():
+    """The attention sweep's cache: 32,768 tokens in 16 chunks of 2048, its first
+    two layers, at three of the swept rho, one call per layer."""
+    w = dataclasses.replace(synth.WORKLOADS["attn32k"], n_layers=2)
+    log(f"case attn32k first two layers, T={w.n_tokens}")
+    _isolated_full_size(w, rhos=(0.05, 0.2, 0.5), n_random=32, check_rebase=False)
+
+
+def test_rebase262k_full_size_sampled():
+    """The rebase sweep's largest cache: 262,144 tokens in 128 chunks of 2048,
+    36 layers x 2 KV heads (4.8 GB of keys: byte offsets past 2^32), every chunk
+    moved on all three axes.  Sampled rows (each chunk's first and last token,
+    the last plane, random rows) against the oracle's Eq. 3 per row."""
+    w = synth.WORKLOADS["rebase262k"]
+    P, T, D = w.n_layers * w.n_kv_heads, w.n_tokens, w.head_dim
+    log(f"case rebase262k full size, {P} planes x {T} tokens")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(262)
+    K = torch.randn((P, T, D), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    rng = np.random.default_rng(262)
+    cs = w.chunk_start
+    nc = len(cs) - 1
+    toks = np.concatenate([cs[:-1], cs[1:] - 1, rng.integers(0, T, 4096), T - 1 - np.arange(64)])
+    planes = np.concatenate([rng.integers(0, P, 2 * nc), rng.integers(0, P, 4096), np.full(64, P - 1)])
+    pi, ti = torch.from_numpy(planes).cuda(), torch.from_numpy(toks).cuda()
+    before = to_host(K[pi, ti], "bf16")
+    b = B()
+    off = synth.chunk_offsets(w)
+    b.compose_rebase_k(b.Geo.from_workload(w), K.view(w.n_layers, w.n_kv_heads, T, D), off)
+    after = to_host(K[pi, ti], "bf16")
+    th, sg = theta_sigma(w)
+    chunk = np.searchsorted(cs, toks, side="right") - 1
+    want = oracle.rebase.rebase_tokens_stored(before[None], "bf16", off[chunk], th, sg)[0]
+    g_, o_ = dec(after, "bf16"), dec(want, "bf16")
+    assert np.all(np.abs(g_ - o_) <= ulp(o_, "bf16") + 2.0 ** -20 * pair_norm(o_))
+    assert not np.array_equal(after, before)
+
+
 def test_more_than_1024_row_tiles():
     """G = 32 puts 8 selected rows in a row tile: 9000 selected rows make 1125
     row tiles, more than the planning workgroup's 1024 threads, with cut row
