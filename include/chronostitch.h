@@ -17,6 +17,9 @@
  *    the same thread).
  *  - Argument errors are detected before anything is enqueued and before any
  *    HIP runtime call, so a rejected call leaves device memory untouched.
+ *    The same holds for a call whose kernel launches would exceed the GPU's
+ *    grid limits (caches of tens of millions of tokens per call): every launch
+ *    of the call is sized first, and such a call returns CS_ERR_UNSUPPORTED.
  *  - DEVICE pointers are device memory of the current HIP device; HOST
  *    pointers are read (or written) before the call returns.  The caller
  *    owns every buffer; the library allocates no device memory.  Scratch

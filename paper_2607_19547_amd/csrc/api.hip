@@ -28,6 +28,13 @@ cs_status check_launch(const char* what) {
   return CS_OK;
 }
 
+cs_status check_grid(int64_t gx, int64_t gy, int64_t gz, int threads, const char* what) {
+  if (gx >= (int64_t(1) << 31) || gx * threads >= (int64_t(1) << 32) || gy > 65535 || gz > 65535)
+    return fail(CS_ERR_UNSUPPORTED, std::string(what) + ": the cache is too large for one launch (grid " +
+                                        std::to_string(gx) + " x " + std::to_string(gy) + " x " + std::to_string(gz) + ")");
+  return CS_OK;
+}
+
 // ------------------------------------------------------------------ tracing
 namespace {
 struct Pending {
@@ -162,6 +169,7 @@ static cs_status rebase_k(const cs_geometry* gp, const Geo& g, const CacheView& 
     return fail(CS_ERR_INVALID_ARGUMENT, "global_coords needs local_coords");
   std::vector<double> theta;
   cs_status st = theta_table(gp, g, &theta);
+  if (!st) st = launch_rebase(g, cv, chunk_offsets, theta.data(), (hipStream_t)stream, true);
   if (st) return st;
   // Coordinate shift (host): p' = p + Delta_c for every token of chunk c.
   if (global_coords) {
@@ -178,6 +186,7 @@ static cs_status rebase_k_tokens(const cs_geometry* gp, const Geo& g, const Cach
   if (!token_offsets) return fail(CS_ERR_INVALID_ARGUMENT, "token_offsets is NULL");
   std::vector<double> theta;
   cs_status st = theta_table(gp, g, &theta);
+  if (!st) st = launch_rebase_tokens(g, cv, token_offsets, theta.data(), (hipStream_t)stream, true);
   if (st) return st;
   return launch_rebase_tokens(g, cv, token_offsets, theta.data(), (hipStream_t)stream);
 }
@@ -200,6 +209,10 @@ static cs_status score_topk(const Geo& g, const CacheView& cv, int32_t score_lay
       scores = (float*)workspace;
     }
   }
+  if (g.n > 0) {
+    cs_status st = launch_score_select(g, cv, score_layer, k_fresh, scores, sel_idx, k, (hipStream_t)stream, true);
+    if (st) return st;
+  }
   *n_sel = k;
   if (g.n == 0) return CS_OK;
   return launch_score_select(g, cv, score_layer, k_fresh, scores, sel_idx, k, (hipStream_t)stream);
@@ -220,9 +233,15 @@ static cs_status attend_scatter(const Geo& g, const CacheView& cv, int32_t layer
   if (cv.paged && p.mfma && !chunks_tile_aligned(g))
     return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
   hipStream_t s = (hipStream_t)stream;
-  cs_status st = launch_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, k_fresh, v_fresh, s);
-  if (st) return st;
-  return launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, false, out, lse, workspace, s);
+  for (int pass = 0; pass < 2; ++pass) {  // sizes of every launch first, then the launches
+    const bool check = pass == 0;
+    cs_status st = launch_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, k_fresh, v_fresh, s, check);
+    if (!st)
+      st = launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, false, out, lse, workspace, s,
+                            check);
+    if (st) return st;
+  }
+  return CS_OK;
 }
 
 // Workspace of the fused-rotary variant: the attention's, then the rotated
@@ -253,10 +272,16 @@ static cs_status attend_scatter_rope(const cs_geometry* gp, const Geo& g, const 
     return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
   hipStream_t s = (hipStream_t)stream;
   void* q_ws = (char*)workspace + att;
-  st = launch_rope_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords, theta.data(),
-                           q_ws, s);
-  if (st) return st;
-  return launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_ws, true, out, lse, workspace, s);
+  for (int pass = 0; pass < 2; ++pass) {  // sizes of every launch first, then the launches
+    const bool check = pass == 0;
+    st = launch_rope_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords,
+                             theta.data(), q_ws, s, check);
+    if (!st)
+      st = launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_ws, true, out, lse, workspace, s,
+                            check);
+    if (st) return st;
+  }
+  return CS_OK;
 }
 
 }  // namespace cs

@@ -83,7 +83,9 @@ static void launch_scatter_rows(const Geo& g, const Rows& rows, int lb, int le, 
 }
 
 cs_status launch_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
-                         const void* kf, const void* vf, hipStream_t s) {
+                         const void* kf, const void* vf, hipStream_t s, bool check_only) {
+  cs_status st = check_grid(65535, le - lb, 1, 256, "scatter");  // grid-stride over at most 65535 workgroups
+  if (st || check_only) return st;
   if (cv.paged) launch_scatter_rows(g, cv.pages<kMaxPages>(g), lb, le, sel, n_sel, kf, vf, s);
   else launch_scatter_rows(g, cv.flat(g), lb, le, sel, n_sel, kf, vf, s);
   return check_launch("scatter launch");
@@ -926,6 +928,21 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call) {
   return p;
 }
 
+// Workgroups of the attention launch and of the combine launch.
+static int64_t mfma_grid(const AttnArgs& a) {
+  // items per queue and layer: at most one per row tile and KV head of the
+  // queue, plus the extra pieces of cut row tiles (bounded by part_cap)
+  const int nq = n_queues(a.Hkv);
+  const int64_t per_q = (a.n_tiles * a.Hkv + a.part_cap + nq - 1) / nq;
+  const int64_t share = kXcds / nq;
+  return (per_q * a.layers + share - 1) / share * kXcds;
+}
+static int64_t combine_grid(const AttnArgs& a) {
+  // cut row tiles lead the longest-first order, and each fills at least
+  // 2 H_kv partial slots
+  return std::min<int64_t>(a.n_tiles, a.part_cap / (2 * a.Hkv)) * a.Hkv * kWaves;
+}
+
 template <int G, typename Rows>
 static void launch_mfma_g(const AttnArgs& a, const Rows& rows, hipStream_t s) {
   static_assert(sizeof(AttnArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
@@ -936,20 +953,11 @@ static void launch_mfma_g(const AttnArgs& a, const Rows& rows, hipStream_t s) {
   }
   {
     TraceScope tr("sel_attn_mfma", s);
-    // items per queue and layer: at most one per row tile and KV head of the
-    // queue, plus the extra pieces of cut row tiles (bounded by part_cap)
-    const int nq = n_queues(a.Hkv);
-    const int64_t per_q = (a.n_tiles * a.Hkv + a.part_cap + nq - 1) / nq;
-    const int64_t share = kXcds / nq;
-    const int64_t grid = (per_q * a.layers + share - 1) / share * kXcds;
-    hipLaunchKernelGGL((sel_attn_mfma<G, Rows>), dim3((unsigned)grid), dim3(kThreads), 0, s, a, rows);
+    hipLaunchKernelGGL((sel_attn_mfma<G, Rows>), dim3((unsigned)mfma_grid(a)), dim3(kThreads), 0, s, a, rows);
   }
   if (a.part_cap > 0) {
-    // cut row tiles lead the longest-first order, and each fills at least
-    // 2 H_kv partial slots
-    const int64_t cut_max = std::min<int64_t>(a.n_tiles, a.part_cap / (2 * a.Hkv));
     TraceScope tr("sel_attn_combine", s);
-    hipLaunchKernelGGL(sel_attn_combine<G>, dim3((unsigned)(cut_max * a.Hkv * kWaves), a.layers), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(sel_attn_combine<G>, dim3((unsigned)combine_grid(a), a.layers), dim3(256), 0, s, a);
   }
 }
 
@@ -988,7 +996,7 @@ bool chunks_tile_aligned(const Geo& g) {
 
 cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv, int lb, int le,
                            const int32_t* sel, int64_t n_sel, const void* qf, bool q_by_slot, void* out, float* lse,
-                           void* ws, hipStream_t s) {
+                           void* ws, hipStream_t s, bool check_only) {
   const int layers = le - lb;
   if (p.mfma) {
     if (cv.paged && !chunks_tile_aligned(g))
@@ -1013,6 +1021,9 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv,
     a.part_cap = p.part_cap;
     a.q_by_slot = q_by_slot ? 1 : 0;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g.D));
+    cs_status stg = check_grid(mfma_grid(a), 1, 1, kThreads, "selective attention");
+    if (!stg && a.part_cap > 0) stg = check_grid(combine_grid(a), layers, 1, 256, "partial combine");
+    if (stg || check_only) return stg;
     const cs_status st = cv.paged ? launch_mfma(g.G, a, cv.pages<kMaxPages>(g), s) : launch_mfma(g.G, a, cv.flat(g), s);
     if (st) return st;
     return check_launch("selective attention launch");
@@ -1033,6 +1044,8 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv,
   a.D = g.D;
   a.lb = lb;
   a.scale = (float)(1.0 / sqrt((double)g.D));
+  const cs_status stg = check_grid(n_sel, g.Hq, layers, 64, "selective attention");
+  if (stg || check_only) return stg;
   if (cv.paged) launch_generic(g, a, cv.pages<kMaxPages>(g), n_sel, layers, s);
   else launch_generic(g, a, cv.flat(g), n_sel, layers, s);
   return check_launch("generic attention launch");

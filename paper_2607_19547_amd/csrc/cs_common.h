@@ -14,6 +14,10 @@ namespace cs {
 void set_error(const std::string& msg);
 cs_status fail(cs_status code, const std::string& msg);
 cs_status check_launch(const char* what);
+// A launch of gx x gy x gz workgroups of `threads` work-items within the
+// hardware's grid limits (work-items along x below 2^32, gx below 2^31, gy and
+// gz at most 65535); CS_ERR_UNSUPPORTED otherwise.
+cs_status check_grid(int64_t gx, int64_t gy, int64_t gz, int threads, const char* what);
 
 // ------------------------------------------------------------------ tracing
 // Launch helper: brackets a kernel launch with trace events when tracing is on.
@@ -204,14 +208,16 @@ struct CacheView {
 };
 
 // ------------------------------------------------------------------ launches (per source file)
+// Each launcher with check_only set validates its launch sizes and enqueues
+// nothing, so that an entry point can reject a call before any device work.
 cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* offsets, const double* theta,
-                        hipStream_t s);
+                        hipStream_t s, bool check_only = false);
 cs_status launch_rebase_tokens(const Geo& g, const CacheView& cv, const int32_t* token_offsets, const double* theta,
-                               hipStream_t s);
+                               hipStream_t s, bool check_only = false);
 cs_status launch_score_select(const Geo& g, const CacheView& cv, int score_layer, const void* k_fresh, float* scores,
-                              int32_t* sel, int64_t k_sel, hipStream_t s);
+                              int32_t* sel, int64_t k_sel, hipStream_t s, bool check_only = false);
 cs_status launch_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel,
-                         int64_t n_sel, const void* kf, const void* vf, hipStream_t s);
+                         int64_t n_sel, const void* kf, const void* vf, hipStream_t s, bool check_only = false);
 
 struct AttnPlan {
   bool mfma;            // bf16, D = 128, 32 % G == 0
@@ -226,9 +232,9 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call);
 bool chunks_tile_aligned(const Geo& g);
 cs_status launch_attention(const Geo& g, const AttnPlan& plan, const CacheView& cv,
                            int lb, int le, const int32_t* sel, int64_t n_sel, const void* qf,
-                           bool q_by_slot, void* out, float* lse, void* ws, hipStream_t s);
+                           bool q_by_slot, void* out, float* lse, void* ws, hipStream_t s, bool check_only = false);
 cs_status launch_rope_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
                               const void* q_pre, const void* k_pre, const void* v_new, const int32_t* coords,
-                              const double* theta, void* q_ws, hipStream_t s);
+                              const double* theta, void* q_ws, hipStream_t s, bool check_only = false);
 
 }  // namespace cs

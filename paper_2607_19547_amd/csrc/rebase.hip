@@ -305,8 +305,13 @@ static void launch_tok_generic(const Geo& g, const RebaseTokArgs<256>& a, const 
 }
 
 cs_status launch_rebase_tokens(const Geo& g, const CacheView& cv, const int32_t* off, const double* theta,
-                               hipStream_t s) {
-  if (g.dtype == CS_BF16 && g.D == 128) {
+                               hipStream_t s, bool check_only) {
+  const int64_t planes = (int64_t)g.L * g.Hkv;
+  const bool fast = g.dtype == CS_BF16 && g.D == 128;
+  cs_status st = fast ? check_grid((g.T + kTokTB - 1) / kTokTB, (planes + kTokPG - 1) / kTokPG, 1, 256, "per-token rebase")
+                      : check_grid(g.T, planes, 1, 64, "per-token rebase");
+  if (st || check_only) return st;
+  if (fast) {
     RebaseTokArgs<64> a;
     fill_tok_args(a, g, off, theta);
     if (cv.paged) launch_tok_fast(a, cv.pages<kMaxPages>(g), s);
@@ -322,7 +327,7 @@ cs_status launch_rebase_tokens(const Geo& g, const CacheView& cv, const int32_t*
 
 // ---------------------------------------------------------------- host launcher
 cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, const double* theta,
-                        hipStream_t s) {
+                        hipStream_t s, bool check_only) {
   std::vector<int> todo;
   for (int c = 0; c < g.N; ++c)
     if (off[3 * c] || off[3 * c + 1] || off[3 * c + 2]) todo.push_back(c);
@@ -340,15 +345,22 @@ cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, c
       const int c = todo[b + q];
       maxlen = std::max<int>(maxlen, (int)(g.cs[c + 1] - g.cs[c]));
     }
+    // contiguous: token blocks of the longest chunk; paged: row runs of the largest chunk buffer
+    const int64_t tb_fast = cv.paged ? ((int64_t)planes * maxlen + kFastPG * kFastTB - 1) / (kFastPG * kFastTB)
+                                     : (maxlen + kFastTB - 1) / kFastTB;
+    const int64_t pg_fast = cv.paged ? 1 : (planes + kFastPG - 1) / kFastPG;
+    const int64_t tb_gen = (maxlen + kGenTB - 1) / kGenTB;
+    cs_status st = fast ? check_grid(tb_fast * pg_fast * nc, 1, 1, 256, "rebase")
+                        : check_grid(tb_gen * planes, nc, 1, 256, "rebase");
+    if (st) return st;
+    if (check_only) continue;
     if (fast) {
       RebaseFastArgs a;
       a.T = g.T;
       a.planes = planes;
       a.sec0 = g.sec[0];
       a.sec01 = g.sec[0] + g.sec[1];
-      // contiguous: token blocks of the longest chunk; paged: row runs of the largest chunk buffer
-      a.tblocks = cv.paged ? (int)(((int64_t)planes * maxlen + kFastPG * kFastTB - 1) / (kFastPG * kFastTB))
-                           : (maxlen + kFastTB - 1) / kFastTB;
+      a.tblocks = (int)tb_fast;
       a.nc = nc;
       a.paged = cv.paged ? 1 : 0;
       for (int i = 0; i < 64; ++i) a.theta[i] = theta[i];
@@ -358,9 +370,8 @@ cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, c
         a.len[q] = (int)(g.cs[c + 1] - g.cs[c]);
         for (int x = 0; x < 3; ++x) a.off[q][x] = off[3 * c + x];
       }
-      const int pgroups = cv.paged ? 1 : (planes + kFastPG - 1) / kFastPG;
       TraceScope tr("rebase_bf16_d128", s);
-      hipLaunchKernelGGL(rebase_bf16_d128, dim3((unsigned)((int64_t)a.tblocks * pgroups * nc)), dim3(256), 0, s, a);
+      hipLaunchKernelGGL(rebase_bf16_d128, dim3((unsigned)(tb_fast * pg_fast * nc)), dim3(256), 0, s, a);
     } else {
       RebaseGenArgs a;
       a.T = g.T;
@@ -369,7 +380,7 @@ cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, c
       a.P = g.P;
       a.sec0 = g.sec[0];
       a.sec01 = g.sec[0] + g.sec[1];
-      a.tblocks = (maxlen + kGenTB - 1) / kGenTB;
+      a.tblocks = (int)tb_gen;
       a.paged = cv.paged ? 1 : 0;
       for (int i = 0; i < g.P; ++i) a.theta[i] = theta[i];
       for (int q = 0; q < nc; ++q) {
@@ -384,7 +395,7 @@ cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, c
       else
         hipLaunchKernelGGL(rebase_generic<float>, dim3(a.tblocks * planes, nc), dim3(256), 0, s, a);
     }
-    cs_status st = check_launch("rebase kernel launch");
+    st = check_launch("rebase kernel launch");
     if (st) return st;
   }
   return CS_OK;

@@ -195,8 +195,12 @@ static void launch_rs_generic(const Geo& g, const RopeScatterGenArgs& a, const R
 
 cs_status launch_rope_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
                               const void* q_pre, const void* k_pre, const void* v_new, const int32_t* coords,
-                              const double* theta, void* q_ws, hipStream_t s) {
-  if (g.dtype == CS_BF16 && g.D == 128) {
+                              const double* theta, void* q_ws, hipStream_t s, bool check_only) {
+  const bool fast = g.dtype == CS_BF16 && g.D == 128;
+  const cs_status stg = fast ? check_grid((n_sel + kRsTok - 1) / kRsTok, le - lb, 1, 256, "rope scatter")
+                             : check_grid(n_sel, le - lb, 1, 64, "rope scatter");
+  if (stg || check_only) return stg;
+  if (fast) {
     RopeScatterArgs a;
     a.q_ws = (uint16_t*)q_ws;
     a.q_pre = (const uint16_t*)q_pre;

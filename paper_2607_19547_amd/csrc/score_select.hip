@@ -174,7 +174,10 @@ static void launch_score(const Geo& g, const Rows& rows, int score_layer, const 
 }
 
 cs_status launch_score_select(const Geo& g, const CacheView& cv, int score_layer, const void* k_fresh, float* scores,
-                              int32_t* sel, int64_t k_sel, hipStream_t s) {
+                              int32_t* sel, int64_t k_sel, hipStream_t s, bool check_only) {
+  const bool fast = g.dtype == CS_BF16 && g.D == 128;
+  cs_status st0 = check_grid(fast ? (g.n + 15) / 16 : (g.n + 3) / 4, 1, 1, 256, "deviation score");
+  if (st0 || check_only) return st0;
   if (cv.paged) launch_score(g, cv.pages<kMaxPages>(g), score_layer, k_fresh, scores, s);
   else launch_score(g, cv.flat(g), score_layer, k_fresh, scores, s);
   cs_status st = check_launch("deviation score launch");

@@ -198,3 +198,18 @@ def test_paged_limits(built_lib):
     code, _ = _code(b.selective_attend_scatter_rope_paged, q, [FAKE] * 2, [FAKE] * 2, 0, 1, FAKE, 4, FAKE, FAKE, FAKE,
                     FAKE, FAKE, workspace=FAKE, stream=0)
     assert code == b.CS_ERR_UNSUPPORTED
+
+
+def test_launch_sizes_beyond_the_grid_limits_are_rejected(built_lib):
+    """A cache too large for one launch is refused with CS_ERR_UNSUPPORTED before
+    anything is enqueued (every launch of a call is sized first)."""
+    T = (1 << 31) - 128
+    huge = b.Geo(36, 16, 2, 128, (16, 24, 24), "bf16", [0, 64, T])
+    code, text = _code(b.compose_rebase_k, huge, FAKE, np.array([[0, 0, 0], [5, 0, 0]]), stream=0)
+    assert code == b.CS_ERR_UNSUPPORTED and "too large" in text
+    code, text = _code(b.score_deviation_topk, huge, FAKE, 0, FAKE, 0.5, FAKE, FAKE, stream=0)
+    assert code == b.CS_ERR_UNSUPPORTED and "too large" in text
+    big = (1 << 27)
+    code, text = _code(b.selective_attend_scatter, huge, FAKE, FAKE, 0, 1, FAKE, big, FAKE, FAKE, FAKE, FAKE,
+                       stream=0)
+    assert code == b.CS_ERR_UNSUPPORTED and "too large" in text
