@@ -481,8 +481,8 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=No
     reb_n, reb_ms = tr.get("rebase_bf16_d128", (0, 0.0))
     reb_avg_s = reb_ms / max(reb_n, 1) / 1e3
     reb_gbps = r["rebase_bytes"] / reb_avg_s / 1e9 if reb_n else None
-    # whole attention stage per layer call: scatter + attention + combine
-    stage = sum(tr.get(k, (0, 0.0))[1] for k in ("scatter_rows", "sel_attn_mfma", "sel_attn_combine"))
+    # whole attention stage per layer call: scatter (with the plan, in one launch) + attention + combine
+    stage = sum(tr.get(k, (0, 0.0))[1] for k in ("plan_scatter", "scatter_rows", "sel_attn_mfma", "sel_attn_combine"))
     stage_tflops = w.n_layers * r["attn_flops_per_layer"] / (stage / steps / 1e3) / 1e12 if stage else None
     line = {
         "metric": "compose ms/65k-token cache; rebase GB/s (% HBM peak); sel-attn TFLOP/s (% MFMA)",

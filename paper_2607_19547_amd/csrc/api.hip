@@ -233,12 +233,11 @@ static cs_status attend_scatter(const Geo& g, const CacheView& cv, int32_t layer
   if (cv.paged && p.mfma && !chunks_tile_aligned(g))
     return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
   hipStream_t s = (hipStream_t)stream;
+  // the scatter of the fresh rows runs inside the attention's first launch
+  const ScatterJob job{k_fresh, v_fresh};
   for (int pass = 0; pass < 2; ++pass) {  // sizes of every launch first, then the launches
-    const bool check = pass == 0;
-    cs_status st = launch_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, k_fresh, v_fresh, s, check);
-    if (!st)
-      st = launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, false, out, lse, workspace, s,
-                            check);
+    cs_status st = launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, false, out, lse,
+                                    workspace, s, pass == 0, &job);
     if (st) return st;
   }
   return CS_OK;

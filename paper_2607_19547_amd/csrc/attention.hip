@@ -37,59 +37,78 @@ namespace cs {
 
 // ============================================================== scatter
 // K[layer][h][t] <- K_fresh[layer][h][t - s1] and the same for V, for every
-// selected token t; cache rows are reached through the row map.  W is the
-// bytes one thread moves (16 when a row is a whole number of 16-byte words).
+// selected token t and every layer of the call; cache rows are reached through
+// the row map.  W is the bytes one thread moves (16 when a row is a whole
+// number of 16-byte words).  Work items first, first + stride, ...
+struct ScatterArgs {
+  const char* kf;
+  const char* vf;
+  const int32_t* sel;
+  int64_t n_sel, T, n, cs1;
+  int Hkv, row_bytes, lb, layers;
+};
+
 template <int W, typename Rows>
-__global__ __launch_bounds__(256) void scatter_rows(const Rows rows, const char* __restrict__ kf,
-                                                    const char* __restrict__ vf,
-                                                    const int32_t* __restrict__ sel, int64_t n_sel,
-                                                    int64_t T, int64_t n, int64_t cs1, int Hkv,
-                                                    int row_bytes, int lb) {
+__device__ __forceinline__ void scatter_body(const Rows& rows, const ScatterArgs& a, int64_t first, int64_t stride) {
   typedef typename std::conditional<W == 16, u32x4, uint32_t>::type word;
-  const int layer = lb + blockIdx.y;
-  const int words = row_bytes / W;
-  const int64_t total = (int64_t)Hkv * n_sel * words;
-  for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < total;
-       w += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(w % words);
-    const int64_t hm = w / words;
-    const int64_t m = hm % n_sel;
-    const int h = (int)(hm / n_sel);
-    const int64_t t = sel[m];
-    if (t < cs1 || t >= T) continue;  // out-of-contract index: never write outside the cache
+  const int words = a.row_bytes / W;
+  const int64_t per_layer = (int64_t)a.Hkv * a.n_sel * words;
+  const int64_t total = per_layer * a.layers;
+  for (int64_t w = first; w < total; w += stride) {
+    const int lr = (int)(w / per_layer);
+    const int64_t x = w - lr * per_layer;
+    const int c = (int)(x % words);
+    const int64_t hm = x / words;
+    const int64_t m = hm % a.n_sel;
+    const int h = (int)(hm / a.n_sel);
+    const int layer = a.lb + lr;
+    const int64_t t = a.sel[m];
+    if (t < a.cs1 || t >= a.T) continue;  // out-of-contract index: never write outside the cache
     char *kr, *vr;
-    rows.kv_rows((int64_t)layer * Hkv + h, t, row_bytes, kr, vr);
-    const int64_t src = (((int64_t)layer * Hkv + h) * n + (t - cs1)) * row_bytes + W * c;
-    *(word*)(kr + W * c) = *(const word*)(kf + src);
-    *(word*)(vr + W * c) = *(const word*)(vf + src);
+    rows.kv_rows((int64_t)layer * a.Hkv + h, t, a.row_bytes, kr, vr);
+    const int64_t src = (((int64_t)layer * a.Hkv + h) * a.n + (t - a.cs1)) * a.row_bytes + W * c;
+    *(word*)(kr + W * c) = *(const word*)(a.kf + src);
+    *(word*)(vr + W * c) = *(const word*)(a.vf + src);
   }
 }
 
-template <typename Rows>
-static void launch_scatter_rows(const Geo& g, const Rows& rows, int lb, int le, const int32_t* sel, int64_t n_sel,
-                                const void* kf, const void* vf, hipStream_t s) {
-  static_assert(sizeof(Rows) + 96 <= 4096, "kernel arguments within 4 KB");
-  const int row_bytes = g.D * g.esize;
-  const bool wide = row_bytes % 16 == 0;
-  const int64_t total = (int64_t)g.Hkv * n_sel * (wide ? row_bytes / 16 : row_bytes / 4);
-  const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 65535);
-  TraceScope tr("scatter_rows", s);
-  if (wide)
-    hipLaunchKernelGGL((scatter_rows<16, Rows>), dim3(blocks, le - lb), dim3(256), 0, s, rows, (const char*)kf,
-                       (const char*)vf, sel, n_sel, g.T, g.n, g.cs1, g.Hkv, row_bytes, lb);
-  else
-    hipLaunchKernelGGL((scatter_rows<4, Rows>), dim3(blocks, le - lb), dim3(256), 0, s, rows, (const char*)kf,
-                       (const char*)vf, sel, n_sel, g.T, g.n, g.cs1, g.Hkv, row_bytes, lb);
+template <int W, typename Rows>
+__global__ __launch_bounds__(256) void scatter_rows(const Rows rows, const ScatterArgs a) {
+  scatter_body<W>(rows, a, (int64_t)blockIdx.x * 256 + threadIdx.x, (int64_t)gridDim.x * 256);
 }
 
-cs_status launch_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
-                         const void* kf, const void* vf, hipStream_t s, bool check_only) {
-  cs_status st = check_grid(65535, le - lb, 1, 256, "scatter");  // grid-stride over at most 65535 workgroups
-  if (st || check_only) return st;
-  if (cv.paged) launch_scatter_rows(g, cv.pages<kMaxPages>(g), lb, le, sel, n_sel, kf, vf, s);
-  else launch_scatter_rows(g, cv.flat(g), lb, le, sel, n_sel, kf, vf, s);
-  return check_launch("scatter launch");
+static ScatterArgs scatter_args(const Geo& g, int lb, int le, const int32_t* sel, int64_t n_sel, const void* kf,
+                                const void* vf) {
+  ScatterArgs a;
+  a.kf = (const char*)kf;
+  a.vf = (const char*)vf;
+  a.sel = sel;
+  a.n_sel = n_sel;
+  a.T = g.T;
+  a.n = g.n;
+  a.cs1 = g.cs1;
+  a.Hkv = g.Hkv;
+  a.row_bytes = g.D * g.esize;
+  a.lb = lb;
+  a.layers = le - lb;
+  return a;
 }
+static int scatter_word(const ScatterArgs& a) { return a.row_bytes % 16 == 0 ? 16 : 4; }
+static int64_t scatter_items(const ScatterArgs& a) {
+  return (int64_t)a.Hkv * a.n_sel * (a.row_bytes / scatter_word(a)) * a.layers;
+}
+
+template <typename Rows>
+static void launch_scatter_rows(const ScatterArgs& a, const Rows& rows, hipStream_t s) {
+  static_assert(sizeof(Rows) + sizeof(ScatterArgs) <= 4096, "kernel arguments within 4 KB");
+  const unsigned blocks = (unsigned)std::min<int64_t>((scatter_items(a) + 255) / 256, 65535);
+  TraceScope tr("scatter_rows", s);
+  if (scatter_word(a) == 16)
+    hipLaunchKernelGGL((scatter_rows<16, Rows>), dim3(blocks), dim3(256), 0, s, rows, a);
+  else
+    hipLaunchKernelGGL((scatter_rows<4, Rows>), dim3(blocks), dim3(256), 0, s, rows, a);
+}
+
 
 // ============================================================== MFMA attention
 constexpr int kKT = 64;                  // keys per tile
@@ -258,9 +277,14 @@ __device__ __forceinline__ int block_scan(int x, int* wsum, int* base) {
 // Builds the work plan of one call (one workgroup of 1024 threads).  Thread t
 // handles row tiles t, t + 1024, ... in every pass, so it reads back only
 // what it wrote itself.
-__global__ __launch_bounds__(1024) void plan_items(const int32_t* __restrict__ sel, int64_t n_sel, int64_t n_tiles,
-                                                   int RT, int64_t T, int Hkv, int layers, int part_cap,
-                                                   int* __restrict__ plan) {
+struct PlanArgs {
+  const int32_t* sel;
+  int64_t n_sel, n_tiles, T;
+  int RT, Hkv, layers, part_cap;
+  int* plan;
+};
+__device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_t n_tiles, int RT, int64_t T, int Hkv,
+                          int layers, int part_cap, int* __restrict__ plan) {
   __shared__ int red[16];
   __shared__ int wsum[16];
   __shared__ int s_base;
@@ -354,6 +378,22 @@ __global__ __launch_bounds__(1024) void plan_items(const int32_t* __restrict__ s
     pv.hdr[11] = nj;
     pv.hdr[12] = per_q;
   }
+}
+
+__global__ __launch_bounds__(1024) void plan_items(const PlanArgs p) {
+  plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.plan);
+}
+
+// The plan (workgroup 0) and the scatter of the call's fresh rows (the other
+// workgroups) in one launch: the two are independent, and the attention that
+// follows needs both.
+template <int W, typename Rows>
+__global__ __launch_bounds__(1024) void plan_scatter(const PlanArgs p, const Rows rows, const ScatterArgs sa) {
+  if (blockIdx.x == 0) {
+    plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.plan);
+    return;
+  }
+  scatter_body<W>(rows, sa, (int64_t)(blockIdx.x - 1) * 1024 + threadIdx.x, (int64_t)(gridDim.x - 1) * 1024);
 }
 
 template <int G, typename Rows>
@@ -943,13 +983,34 @@ static int64_t combine_grid(const AttnArgs& a) {
   return std::min<int64_t>(a.n_tiles, a.part_cap / (2 * a.Hkv)) * a.Hkv * kWaves;
 }
 
+static int64_t plan_scatter_blocks(const ScatterArgs& sa) {
+  return 1 + std::min<int64_t>((scatter_items(sa) + 1023) / 1024, 16384);
+}
+
 template <int G, typename Rows>
-static void launch_mfma_g(const AttnArgs& a, const Rows& rows, hipStream_t s) {
+static void launch_mfma_g(const AttnArgs& a, const Rows& rows, const ScatterArgs* sa, hipStream_t s) {
   static_assert(sizeof(AttnArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
-  {
+  static_assert(sizeof(PlanArgs) + sizeof(Rows) + sizeof(ScatterArgs) <= 4096, "kernel arguments within 4 KB");
+  PlanArgs pa;
+  pa.sel = a.sel;
+  pa.n_sel = a.n_sel;
+  pa.n_tiles = a.n_tiles;
+  pa.T = a.T;
+  pa.RT = kWaves * (32 / G);
+  pa.Hkv = a.Hkv;
+  pa.layers = a.layers;
+  pa.part_cap = a.part_cap;
+  pa.plan = a.plan;
+  if (sa) {
+    TraceScope tr("plan_scatter", s);
+    const unsigned blocks = (unsigned)plan_scatter_blocks(*sa);
+    if (scatter_word(*sa) == 16)
+      hipLaunchKernelGGL((plan_scatter<16, Rows>), dim3(blocks), dim3(1024), 0, s, pa, rows, *sa);
+    else
+      hipLaunchKernelGGL((plan_scatter<4, Rows>), dim3(blocks), dim3(1024), 0, s, pa, rows, *sa);
+  } else {
     TraceScope tr("plan_items", s);
-    hipLaunchKernelGGL(plan_items, dim3(1), dim3(1024), 0, s, a.sel, a.n_sel, a.n_tiles, kWaves * (32 / G), a.T,
-                       a.Hkv, a.layers, a.part_cap, a.plan);
+    hipLaunchKernelGGL(plan_items, dim3(1), dim3(1024), 0, s, pa);
   }
   {
     TraceScope tr("sel_attn_mfma", s);
@@ -962,14 +1023,14 @@ static void launch_mfma_g(const AttnArgs& a, const Rows& rows, hipStream_t s) {
 }
 
 template <typename Rows>
-static cs_status launch_mfma(int G, const AttnArgs& a, const Rows& rows, hipStream_t s) {
+static cs_status launch_mfma(int G, const AttnArgs& a, const Rows& rows, const ScatterArgs* sa, hipStream_t s) {
   switch (G) {
-    case 1: launch_mfma_g<1>(a, rows, s); break;
-    case 2: launch_mfma_g<2>(a, rows, s); break;
-    case 4: launch_mfma_g<4>(a, rows, s); break;
-    case 8: launch_mfma_g<8>(a, rows, s); break;
-    case 16: launch_mfma_g<16>(a, rows, s); break;
-    case 32: launch_mfma_g<32>(a, rows, s); break;
+    case 1: launch_mfma_g<1>(a, rows, sa, s); break;
+    case 2: launch_mfma_g<2>(a, rows, sa, s); break;
+    case 4: launch_mfma_g<4>(a, rows, sa, s); break;
+    case 8: launch_mfma_g<8>(a, rows, sa, s); break;
+    case 16: launch_mfma_g<16>(a, rows, sa, s); break;
+    case 32: launch_mfma_g<32>(a, rows, sa, s); break;
     default: return fail(CS_ERR_UNSUPPORTED, "MFMA attention needs H_q/H_kv dividing 32");
   }
   return CS_OK;
@@ -996,8 +1057,10 @@ bool chunks_tile_aligned(const Geo& g) {
 
 cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv, int lb, int le,
                            const int32_t* sel, int64_t n_sel, const void* qf, bool q_by_slot, void* out, float* lse,
-                           void* ws, hipStream_t s, bool check_only) {
+                           void* ws, hipStream_t s, bool check_only, const ScatterJob* job) {
   const int layers = le - lb;
+  ScatterArgs sa;
+  if (job) sa = scatter_args(g, lb, le, sel, n_sel, job->kf, job->vf);
   if (p.mfma) {
     if (cv.paged && !chunks_tile_aligned(g))
       return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
@@ -1024,7 +1087,9 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv,
     cs_status stg = check_grid(mfma_grid(a), 1, 1, kThreads, "selective attention");
     if (!stg && a.part_cap > 0) stg = check_grid(combine_grid(a), layers, 1, 256, "partial combine");
     if (stg || check_only) return stg;
-    const cs_status st = cv.paged ? launch_mfma(g.G, a, cv.pages<kMaxPages>(g), s) : launch_mfma(g.G, a, cv.flat(g), s);
+    const ScatterArgs* sp = job ? &sa : nullptr;
+    const cs_status st = cv.paged ? launch_mfma(g.G, a, cv.pages<kMaxPages>(g), sp, s)
+                                  : launch_mfma(g.G, a, cv.flat(g), sp, s);
     if (st) return st;
     return check_launch("selective attention launch");
   }
@@ -1046,6 +1111,10 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv,
   a.scale = (float)(1.0 / sqrt((double)g.D));
   const cs_status stg = check_grid(n_sel, g.Hq, layers, 64, "selective attention");
   if (stg || check_only) return stg;
+  if (job) {  // the scatter first: the attention reads the repaired rows
+    if (cv.paged) launch_scatter_rows(sa, cv.pages<kMaxPages>(g), s);
+    else launch_scatter_rows(sa, cv.flat(g), s);
+  }
   if (cv.paged) launch_generic(g, a, cv.pages<kMaxPages>(g), n_sel, layers, s);
   else launch_generic(g, a, cv.flat(g), n_sel, layers, s);
   return check_launch("generic attention launch");

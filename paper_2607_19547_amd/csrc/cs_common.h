@@ -216,8 +216,6 @@ cs_status launch_rebase_tokens(const Geo& g, const CacheView& cv, const int32_t*
                                hipStream_t s, bool check_only = false);
 cs_status launch_score_select(const Geo& g, const CacheView& cv, int score_layer, const void* k_fresh, float* scores,
                               int32_t* sel, int64_t k_sel, hipStream_t s, bool check_only = false);
-cs_status launch_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel,
-                         int64_t n_sel, const void* kf, const void* vf, hipStream_t s, bool check_only = false);
 
 struct AttnPlan {
   bool mfma;            // bf16, D = 128, 32 % G == 0
@@ -230,9 +228,16 @@ struct AttnPlan {
 AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call);
 // Every chunk starts at a multiple of the 64-key tile (a paged cache on the MFMA path needs it).
 bool chunks_tile_aligned(const Geo& g);
+// The fresh K/V rows the attention launch also scatters into the cache
+// before it reads it (the plain scatter of selective_attend_scatter).
+struct ScatterJob {
+  const void* kf;
+  const void* vf;
+};
 cs_status launch_attention(const Geo& g, const AttnPlan& plan, const CacheView& cv,
                            int lb, int le, const int32_t* sel, int64_t n_sel, const void* qf,
-                           bool q_by_slot, void* out, float* lse, void* ws, hipStream_t s, bool check_only = false);
+                           bool q_by_slot, void* out, float* lse, void* ws, hipStream_t s, bool check_only = false,
+                           const ScatterJob* job = nullptr);
 cs_status launch_rope_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
                               const void* q_pre, const void* k_pre, const void* v_new, const int32_t* coords,
                               const double* theta, void* q_ws, hipStream_t s, bool check_only = false);
