@@ -809,33 +809,49 @@ __global__ __launch_bounds__(256) void sel_attn_combine(const AttnArgs a) {
   const int layer = a.lb + blockIdx.y;
   const int64_t slot0 = (int64_t)blockIdx.y * a.part_cap + pv.ppre[oi] + kvh * nsp;
   const int64_t m0 = (a.n_tiles - 1 - oi) * RT;
-  for (int idx = threadIdx.x; idx < 32 * 32; idx += blockDim.x) {
-    const int qv = 32 * w + (idx >> 5), d4 = idx & 31;  // query vector qv of the tile: row qv / G, head qv % G
-    const int64_t m = m0 + qv / G;
-    if (m >= a.n_sel) continue;
-    const int t = a.sel[m];
-    if (t < a.cs1 || t >= a.T) continue;  // not a later-chunk token: no output (as in the direct path)
-    const int h = kvh * G + qv % G;
-    float M = -INFINITY;
-    for (int p = 0; p < nsp; ++p) M = fmaxf(M, a.part_ml[((slot0 + p) * kQPerWG + qv) * 4]);
-    float Lsum = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int p = 0; p < nsp; ++p) {
-      const int64_t slot = slot0 + p;
-      const f32x4 ml = *(const f32x4*)(a.part_ml + (slot * kQPerWG + qv) * 4);
-      const float wgt = ml[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml[0] - M) * ml[1];
-      Lsum += wgt;
-      const f16x4 po = *(const f16x4*)(a.part + (slot * kQPerWG + qv) * 128 + 4 * d4);
-      acc += (wgt * __builtin_ldexpf(1.f, (int)ml[2])) * __builtin_convertvector(po, f32x4);
+  // thread: query vector qv of the tile (row qv / G, head qv % G), dims 16 d16 .. 16 d16 + 15
+  const int qv = 32 * w + (threadIdx.x >> 3), d16 = threadIdx.x & 7;
+  const int64_t m = m0 + qv / G;
+  if (m >= a.n_sel) return;
+  const int t = a.sel[m];
+  if (t < a.cs1 || t >= a.T) return;  // not a later-chunk token: no output (as in the direct path)
+  const int h = kvh * G + qv % G;
+  const float* ml0 = a.part_ml + (slot0 * kQPerWG + qv) * 4;
+  const uint16_t* po0 = a.part + (slot0 * kQPerWG + qv) * 128 + 16 * d16;
+  constexpr int64_t kSlotMl = kQPerWG * 4, kSlotPo = kQPerWG * 128;  // one partial slot apart
+  float M = -INFINITY;
+#pragma unroll 8
+  for (int p = 0; p < nsp; ++p) M = fmaxf(M, ml0[p * kSlotMl]);
+  float Lsum = 0.f;
+  f32x4 acc[4] = {};
+  // piece order, several pieces' loads in flight
+#pragma unroll 4
+  for (int p = 0; p < nsp; ++p) {
+    const f32x4 ml = *(const f32x4*)(ml0 + p * kSlotMl);
+    const float wgt = ml[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml[0] - M) * ml[1];
+    Lsum += wgt;
+    const float sw = wgt * __builtin_ldexpf(1.f, (int)ml[2]);
+    const uint16_t* pp = po0 + p * kSlotPo;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const f16x4 po = *(const f16x4*)(pp + 4 * k);
+      acc[k] += sw * __builtin_convertvector(po, f32x4);
     }
-    const float inv = 1.f / Lsum;
-    uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128 + 4 * d4;
-    u32x2 w2;
-    w2[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
-    w2[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
-    *(u32x2*)op = w2;
-    if (a.lse && d4 == 0) a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (M + __log2f(Lsum)) * kLn2;
   }
+  const float inv = 1.f / Lsum;
+  uint16_t* op = a.out + (((int64_t)layer * a.Hq + h) * a.n_sel + m) * 128 + 16 * d16;
+  u32x4 o0, o1;
+  o0[0] = pack_bf16x2(acc[0][0] * inv, acc[0][1] * inv);
+  o0[1] = pack_bf16x2(acc[0][2] * inv, acc[0][3] * inv);
+  o0[2] = pack_bf16x2(acc[1][0] * inv, acc[1][1] * inv);
+  o0[3] = pack_bf16x2(acc[1][2] * inv, acc[1][3] * inv);
+  o1[0] = pack_bf16x2(acc[2][0] * inv, acc[2][1] * inv);
+  o1[1] = pack_bf16x2(acc[2][2] * inv, acc[2][3] * inv);
+  o1[2] = pack_bf16x2(acc[3][0] * inv, acc[3][1] * inv);
+  o1[3] = pack_bf16x2(acc[3][2] * inv, acc[3][3] * inv);
+  *(u32x4*)op = o0;
+  *(u32x4*)(op + 8) = o1;
+  if (a.lse && d16 == 0) a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (M + __log2f(Lsum)) * kLn2;
 }
 
 // ============================================================== generic attention
