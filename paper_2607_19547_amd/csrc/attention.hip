@@ -132,6 +132,7 @@ struct AttnArgs {
   int cs1, Hq, Hkv, lb, layers;
   int part_cap;      // partial slots per layer
   int q_by_slot;     // q is [layers in call][H_q][n_sel][128] (rows in selection order), else [L][H_q][n][128]
+  int desc_off;      // item descriptors in the plan (set by the planning kernel's caller)
   float scale_log2;  // log2(e) / sqrt(D)
 };
 
@@ -216,7 +217,8 @@ constexpr int kXcds = 8;
 
 struct PlanView {
   int* hdr;   // [0, 8) queue counters, [8] nq, [9] S, [10] cut row tiles, [11] most pieces,
-              // [12] items per queue and layer, [13] workgroup rounds placed by position
+              // [12] items per queue and layer, [13] workgroup rounds placed by position,
+              // [14] offset of the item descriptors (ints from the plan's start)
   int* nu;    // [n_tiles] key tiles of row tile i (longest first)
   int* nsp;   // [n_tiles] pieces of row tile i
   int* ppre;  // [n_tiles + 1] first partial slot of row tile i (prefix sums of H_kv x pieces over cut row tiles)
@@ -281,10 +283,11 @@ struct PlanArgs {
   const int32_t* sel;
   int64_t n_sel, n_tiles, T;
   int RT, Hkv, layers, part_cap;
+  int desc_off;  // where the item descriptors start
   int* plan;
 };
 __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_t n_tiles, int RT, int64_t T, int Hkv,
-                          int layers, int part_cap, int* __restrict__ plan) {
+                          int layers, int part_cap, int desc_off, int* __restrict__ plan) {
   __shared__ int red[16];
   __shared__ int wsum[16];
   __shared__ int s_base;
@@ -377,11 +380,33 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
     pv.hdr[10] = n_cut;
     pv.hdr[11] = nj;
     pv.hdr[12] = per_q;
+    pv.hdr[14] = desc_off;
+  }
+  // Item descriptors, one per queue position (the same in every queue and
+  // layer): {row tile, KV head in the queue | piece << 16, first and last key
+  // tile of the piece}.  Cut row tiles are a prefix of the longest-first order,
+  // so piece j of row tile i sits at pj[j] + kvl * cnt_j + i.
+  __syncthreads();
+  int4* desc = (int4*)(plan + desc_off);
+  const int p_end = pv.pj[nj];
+  const int nun = (int)(n_tiles - n_cut);
+  for (int64_t i = tid; i < n_tiles; i += 1024) {
+    const int v = pv.nu[i], np = pv.nsp[i];
+    if (np > 1) {
+      for (int j = 0; j < np; ++j) {
+        const int cnt = (pv.pj[j + 1] - pv.pj[j]) / kvq;
+        const int b = (int)((int64_t)j * v / np), e = (int)((int64_t)(j + 1) * v / np);
+        for (int kvl = 0; kvl < kvq; ++kvl) desc[pv.pj[j] + kvl * cnt + i] = make_int4((int)i, kvl | (j << 16), b, e);
+      }
+    } else {
+      for (int kvl = 0; kvl < kvq; ++kvl)
+        desc[p_end + kvl * nun + (int)(i - n_cut)] = make_int4((int)i, kvl, 0, v);
+    }
   }
 }
 
 __global__ __launch_bounds__(1024) void plan_items(const PlanArgs p) {
-  plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.plan);
+  plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.desc_off, p.plan);
 }
 
 // The plan (workgroup 0) and the scatter of the call's fresh rows (the other
@@ -390,7 +415,7 @@ __global__ __launch_bounds__(1024) void plan_items(const PlanArgs p) {
 template <int W, typename Rows>
 __global__ __launch_bounds__(1024) void plan_scatter(const PlanArgs p, const Rows rows, const ScatterArgs sa) {
   if (blockIdx.x == 0) {
-    plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.plan);
+    plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.desc_off, p.plan);
     return;
   }
   scatter_body<W>(rows, sa, (int64_t)(blockIdx.x - 1) * 1024 + threadIdx.x, (int64_t)(gridDim.x - 1) * 1024);
@@ -451,8 +476,6 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     if (item < 0) return;  // whole workgroup: every queue is empty
   }
   if (item >= total_q) return;  // (placed rounds never reach past the queue)
-  const int kvq = a.Hkv / nq;
-  const int p_end = pv.pj[nj];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q = lane & 31, hi = lane >> 5;
@@ -476,30 +499,11 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
 
   const int lrel = item / per_q;
   const int r = item - lrel * per_q;
-  int oi, piece, kvl;
-  if (r < p_end) {  // piece j of a cut row tile: pj[j] <= r < pj[j + 1]
-    int lo = 0, up = nj;
-    while (up - lo > 1) {
-      const int mid = (lo + up) >> 1;
-      if (pv.pj[mid] <= r) lo = mid;
-      else up = mid;
-    }
-    const int cnt = (pv.pj[lo + 1] - pv.pj[lo]) / kvq;
-    const int local = r - pv.pj[lo];
-    kvl = local / cnt;
-    oi = local - kvl * cnt;
-    piece = lo;
-  } else {  // an uncut row tile
-    const int nun = (int)a.n_tiles - n_cut;
-    const int local = r - p_end;
-    kvl = local / nun;
-    oi = n_cut + (local - kvl * nun);
-    piece = 0;
-  }
-  const int nsp = pv.nsp[oi], nu = pv.nu[oi];
-  if (piece >= nsp) return;  // (never, for an ascending selection)
+  const int4 dsc = *(const int4*)(a.plan + pv.hdr[14] + 4 * r);  // the item's descriptor
+  const int oi = dsc.x, kvl = dsc.y & 0xffff, piece = dsc.y >> 16;
+  const int64_t seg_b = dsc.z, seg_e = dsc.w;
+  const int nsp = pv.nsp[oi];  // for the epilogue
   const int kv = kvl * nq + jq;
-  const int64_t seg_b = (int64_t)piece * nu / nsp, seg_e = (int64_t)(piece + 1) * nu / nsp;
   const bool full = nsp == 1;
   const int64_t tile = a.n_tiles - 1 - oi;
   const int layer = a.lb + lrel;
@@ -979,7 +983,11 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call) {
     return p;
   }
   p.part_cap = (int)std::min<int64_t>(kPartCap, p.n_tiles * g.Hkv * (max_pieces > 1 ? max_pieces : 0));
-  p.ws_fixed_bytes = (plan_ints(p.n_tiles, max_pieces) * sizeof(int) + 255) / 256 * 256;
+  // item descriptors (4 ints each) after the plan's arrays, one per queue position
+  const int nq = n_queues(g.Hkv);
+  const int64_t per_q_bound = (p.n_tiles * g.Hkv + p.part_cap + nq - 1) / nq;
+  p.desc_off = (int)((plan_ints(p.n_tiles, max_pieces) + 3) / 4 * 4);
+  p.ws_fixed_bytes = ((p.desc_off + 4 * per_q_bound) * sizeof(int) + 255) / 256 * 256;
   p.ws_bytes_per_layer = (size_t)p.part_cap * kQPerWG * (128 * sizeof(uint16_t) + 4 * sizeof(float));
   return p;
 }
@@ -1016,6 +1024,7 @@ static void launch_mfma_g(const AttnArgs& a, const Rows& rows, const ScatterArgs
   pa.Hkv = a.Hkv;
   pa.layers = a.layers;
   pa.part_cap = a.part_cap;
+  pa.desc_off = a.desc_off;
   pa.plan = a.plan;
   if (sa) {
     TraceScope tr("plan_scatter", s);
@@ -1099,6 +1108,7 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv,
     a.layers = layers;
     a.part_cap = p.part_cap;
     a.q_by_slot = q_by_slot ? 1 : 0;
+    a.desc_off = p.desc_off;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g.D));
     cs_status stg = check_grid(mfma_grid(a), 1, 1, kThreads, "selective attention");
     if (!stg && a.part_cap > 0) stg = check_grid(combine_grid(a), layers, 1, 256, "partial combine");

@@ -222,6 +222,7 @@ struct AttnPlan {
   int rows_per_tile;    // selected rows per workgroup tile
   int64_t n_tiles;      // per KV head
   int part_cap;         // partial slots per layer
+  int desc_off;         // item descriptors in the plan (ints from its start)
   size_t ws_fixed_bytes;      // per call: tile plan
   size_t ws_bytes_per_layer;  // per layer in the call: partial segments
 };
