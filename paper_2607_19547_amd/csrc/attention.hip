@@ -13,16 +13,19 @@
 // FMA, a lazy running max that rescales only when the max grows by > 2^8),
 // and the probabilities are packed to bf16 directly as the B operand of
 //   O^T += V^T P^T      (V^T read from LDS with transposing loads).
-// K/V tiles reach LDS by buffer->LDS DMA into a 4-slot ring, two tiles ahead
-// of the one being consumed.  Rows are causal in cache order: key j is
-// visible to row t iff j <= t; tiles below every row's limit skip the mask.
+// K/V tiles reach LDS by buffer->LDS DMA into a 4-slot ring: while the
+// probabilities of tile i and the scores of tile i+1 are computed, tile i+3
+// is fetched.  Rows are causal in cache order: key j is visible to row t iff
+// j <= t; tiles below every row's limit skip the mask.
 //
-// Work is scheduled through a device-side queue: a planning kernel lists
-// the (row tile, KV head, key piece) items, longest row tiles first, and one
-// persistent workgroup per CU takes items from an atomic counter.  Row tiles
-// too long for an even schedule are cut into key pieces whose partial
-// (O, max, sum) a combine kernel merges in a fixed order, so results do not
-// depend on timing.
+// Work is scheduled on the device: a planning workgroup (in the same launch
+// as the scatter of the fresh rows) lists the (row tile, KV head, key piece)
+// items, longest row tiles first, with a descriptor per item, and each
+// attention workgroup runs one item: the first three quarters of every queue
+// are dealt by workgroup position, the rest through an atomic counter per
+// queue.  Row tiles too long for an even schedule are cut into key pieces
+// whose partial (O, max, sum) a combine kernel merges in a fixed order, so
+// results do not depend on timing.
 //
 // Generic path: one wavefront per (row, query head), float32 arithmetic, any
 // head_dim <= 512 and either storage dtype.
