@@ -214,7 +214,7 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_bu
 constexpr int kPlanHdr = 16;    // header ints, see PlanView
 constexpr int kPlanCUs = 256;   // CU count S is derived from (a constant: results do not depend on the device)
 constexpr int kItemsPerCU = 6;  // target items per CU when row tiles must be cut
-constexpr int kMinPiece = 16;   // smallest piece: 16 key tiles
+constexpr int kMinPiece = 64;   // smallest piece: 64 key tiles (an item's fixed cost is ~7 tiles)
 constexpr int kPartCap = 2560;  // partial slots per layer, at most
 constexpr int kXcds = 8;
 
