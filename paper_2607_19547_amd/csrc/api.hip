@@ -45,6 +45,9 @@ struct Acc {
   int64_t launches = 0;
   double ms = 0.0;
 };
+// Tracing state is shared by every thread that calls the library; g_trace_mu
+// guards all of it.
+std::mutex g_trace_mu;
 bool g_trace_on = false;
 std::vector<Pending> g_pending;
 std::vector<std::pair<std::string, Acc>> g_acc;
@@ -62,17 +65,24 @@ hipEvent_t take_event() {
 }
 }  // namespace
 
-TraceScope::TraceScope(const char* n, hipStream_t s) : name(n), stream(s), slot(-1) {
+TraceScope::TraceScope(const char* n, hipStream_t s) : name(n), stream(s), a(nullptr), b(nullptr) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
   if (!g_trace_on) return;
-  hipEvent_t a = take_event(), b = take_event();
-  if (!a || !b) return;
+  a = take_event();
+  b = a ? take_event() : nullptr;
+  if (!b) {
+    if (a) g_pool.push_back(a);
+    a = nullptr;
+    return;
+  }
   hipEventRecord(a, s);
-  g_pending.push_back({name, a, b});
-  slot = (int)g_pending.size() - 1;
 }
 
 TraceScope::~TraceScope() {
-  if (slot >= 0) hipEventRecord(g_pending[slot].b, stream);
+  if (!a) return;
+  hipEventRecord(b, stream);
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  g_pending.push_back({name, a, b});
 }
 
 // ------------------------------------------------------------------ geometry
@@ -468,11 +478,18 @@ cs_status selective_attend_scatter_rope_paged(const cs_geometry* gp, void* const
 
 // ------------------------------------------------------------------ tracing exports
 cs_status cs_trace_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
   g_trace_on = on != 0;
   return CS_OK;
 }
 
 cs_status cs_trace_collect(void) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  size_t done = 0;  // entries already added, dropped even when a later one fails
+  struct Drop {
+    size_t& n;
+    ~Drop() { g_pending.erase(g_pending.begin(), g_pending.begin() + n); }
+  } drop{done};
   for (auto& p : g_pending) {
     if (hipEventSynchronize(p.b) != hipSuccess) return fail(CS_ERR_HIP, "hipEventSynchronize failed");
     float ms = 0.f;
@@ -494,14 +511,18 @@ cs_status cs_trace_collect(void) {
     }
     g_pool.push_back(p.a);
     g_pool.push_back(p.b);
+    ++done;
   }
-  g_pending.clear();
   return CS_OK;
 }
 
-int32_t cs_trace_count(void) { return (int32_t)g_acc.size(); }
+int32_t cs_trace_count(void) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  return (int32_t)g_acc.size();
+}
 
 cs_status cs_trace_get(int32_t i, const char** name, int64_t* launches, double* total_ms) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
   if (i < 0 || i >= (int32_t)g_acc.size()) return fail(CS_ERR_INVALID_ARGUMENT, "trace index out of range");
   if (name) *name = g_acc[i].first.c_str();
   if (launches) *launches = g_acc[i].second.launches;
@@ -509,6 +530,9 @@ cs_status cs_trace_get(int32_t i, const char** name, int64_t* launches, double* 
   return CS_OK;
 }
 
-void cs_trace_reset(void) { g_acc.clear(); }
+void cs_trace_reset(void) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  g_acc.clear();
+}
 
 }  // extern "C"

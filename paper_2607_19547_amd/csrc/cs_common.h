@@ -20,13 +20,14 @@ cs_status check_launch(const char* what);
 cs_status check_grid(int64_t gx, int64_t gy, int64_t gz, int threads, const char* what);
 
 // ------------------------------------------------------------------ tracing
-// Launch helper: brackets a kernel launch with trace events when tracing is on.
+// While tracing is on, brackets the launches of its scope with two events on
+// `s`; the pair is handed to the collector once both are recorded.
 struct TraceScope {
   TraceScope(const char* name, hipStream_t s);
   ~TraceScope();
   const char* name;
   hipStream_t stream;
-  int slot;
+  hipEvent_t a, b;  // both null while tracing is off
 };
 
 // ------------------------------------------------------------------ geometry
