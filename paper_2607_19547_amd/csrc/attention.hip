@@ -612,12 +612,15 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
         if (off + 32 > lim) s1[rr] = -INFINITY;
       }
     }
-    // balanced max tree (short dependency chain)
+    // max tree of three-input maxima (16 instructions), eight independent chains first
     float t8[8];
 #pragma unroll
-    for (int rr = 0; rr < 8; ++rr) t8[rr] = fmaxf(fmaxf(s0[rr], s0[rr + 8]), fmaxf(s1[rr], s1[rr + 8]));
-    const float mx = fmaxf(fmaxf(fmaxf(t8[0], t8[1]), fmaxf(t8[2], t8[3])),
-                           fmaxf(fmaxf(t8[4], t8[5]), fmaxf(t8[6], t8[7])));
+    for (int rr = 0; rr < 8; ++rr) t8[rr] = fmaxf(fmaxf(s0[rr], s0[rr + 8]), s1[rr]);
+    float t4[4];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) t4[rr] = fmaxf(fmaxf(t8[2 * rr], t8[2 * rr + 1]), s1[rr + 8]);
+    const float t2a = fmaxf(fmaxf(t4[0], t4[1]), s1[12]), t2b = fmaxf(fmaxf(t4[2], t4[3]), s1[13]);
+    const float mx = fmaxf(fmaxf(fmaxf(t2a, t2b), s1[14]), s1[15]);
     const float mt = pair_max(mx) * sc;
     const bool need = mt > m_use + kRescaleLog2;
     if (__ballot(need)) {
