@@ -216,6 +216,8 @@ constexpr int kPlanCUs = 256;   // CU count S is derived from (a constant: resul
 constexpr int kItemsPerCU = 6;  // target items per CU when row tiles must be cut
 constexpr int kMinPiece = 64;   // smallest piece: 64 key tiles (an item's fixed cost is ~7 tiles)
 constexpr int kPartCap = 2560;  // partial slots per layer, at most
+constexpr int kPlanLdsTiles = 4096;  // row tiles whose plan arrays the planning workgroup keeps in LDS
+constexpr int kPlanLdsPieces = 2049; // most pieces of a row tile (T < 2^23: ceil(ceil(T / 64) / kMinPiece) <= 2048), + 1
 constexpr int kXcds = 8;
 
 struct PlanView {
@@ -294,7 +296,13 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   __shared__ int red[16];
   __shared__ int wsum[16];
   __shared__ int s_base;
+  // the arrays the plan reads back live in LDS when they fit (global memory
+  // otherwise); nsp is also written to the plan for the attention kernels
+  __shared__ int l_nu[kPlanLdsTiles], l_nsp[kPlanLdsTiles], l_pj[kPlanLdsPieces];
   const PlanView pv = plan_view(plan, n_tiles);
+  const bool in_lds = n_tiles <= kPlanLdsTiles;
+  int* const nu = in_lds ? l_nu : pv.nu;
+  int* const nsp = in_lds ? l_nsp : pv.nsp;
   const int tid = threadIdx.x;
   int sum = 0, mx = 0;
   for (int64_t i = tid; i < n_tiles; i += 1024) {
@@ -302,7 +310,7 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
     const int64_t ml = min((t + 1) * RT, n_sel) - 1;
     const int64_t g = min((int64_t)sel[ml], T - 1);
     const int v = g < 0 ? 1 : (int)((g + kKT) / kKT);
-    pv.nu[i] = v;
+    nu[i] = v;
     sum += v;
     mx = max(mx, v);
   }
@@ -320,7 +328,7 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
       if (Sk >= nmax) break;
       int loc = 0;
       for (int64_t i = tid; i < n_tiles; i += 1024) {
-        const int v = pv.nu[i];
+        const int v = nu[i];
         if (v > Sk) loc += (v + Sk - 1) / Sk;
       }
       if ((int64_t)block_reduce(loc, false, red) * Hkv <= part_cap) {
@@ -337,9 +345,10 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
     const int64_t i = b + tid;
     int np = 1;
     if (i < n_tiles) {
-      const int v = pv.nu[i];
+      const int v = nu[i];
       np = v > S ? (v + S - 1) / S : 1;
-      pv.nsp[i] = np;
+      nsp[i] = np;
+      if (in_lds) pv.nsp[i] = np;
       cut += np > 1;
       npmax = max(npmax, np);
     }
@@ -362,20 +371,20 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
       int lo = 0, up = (int)n_tiles;  // first index with nsp <= need
       while (lo < up) {
         const int mid = (lo + up) >> 1;
-        if (pv.nsp[mid] > need) lo = mid + 1;
+        if (nsp[mid] > need) lo = mid + 1;
         else up = mid;
       }
       c = lo;
     }
     const int inc = block_scan(c * kvq, wsum, &s_base);
-    if (j < nj) pv.pj[j + 1] = inc;
+    if (j < nj) pv.pj[j + 1] = l_pj[j + 1] = inc;
   }
   if (tid == 0) {
     const int per_q = s_base + (int)(n_tiles - n_cut) * kvq;
     const int share = kXcds / nq;
     const int rounds = (int)((int64_t)per_q * layers * 3 / 4 / share);  // placed by position
     pv.ppre[0] = 0;
-    pv.pj[0] = 0;
+    pv.pj[0] = l_pj[0] = 0;
     for (int k = 0; k < kXcds; ++k) pv.hdr[k] = rounds * share;  // first item of the dynamic tail
     pv.hdr[13] = rounds;
     pv.hdr[8] = nq;
@@ -391,15 +400,15 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   // so piece j of row tile i sits at pj[j] + kvl * cnt_j + i.
   __syncthreads();
   int4* desc = (int4*)(plan + desc_off);
-  const int p_end = pv.pj[nj];
+  const int p_end = l_pj[nj];
   const int nun = (int)(n_tiles - n_cut);
   for (int64_t i = tid; i < n_tiles; i += 1024) {
-    const int v = pv.nu[i], np = pv.nsp[i];
+    const int v = nu[i], np = nsp[i];
     if (np > 1) {
       for (int j = 0; j < np; ++j) {
-        const int cnt = (pv.pj[j + 1] - pv.pj[j]) / kvq;
+        const int cnt = (l_pj[j + 1] - l_pj[j]) / kvq;
         const int b = (int)((int64_t)j * v / np), e = (int)((int64_t)(j + 1) * v / np);
-        for (int kvl = 0; kvl < kvq; ++kvl) desc[pv.pj[j] + kvl * cnt + i] = make_int4((int)i, kvl | (j << 16), b, e);
+        for (int kvl = 0; kvl < kvq; ++kvl) desc[l_pj[j] + kvl * cnt + i] = make_int4((int)i, kvl | (j << 16), b, e);
       }
     } else {
       for (int kvl = 0; kvl < kvq; ++kvl)

@@ -9,8 +9,9 @@
 // largest bit pattern by a 4-pass, 8-bit MSB-first radix select with LDS
 // histograms, then compacts in index order: every score above the threshold
 // and the first (lowest-index) ties at the threshold, so the output is
-// ascending and exactly k long.  All counts are order independent, so the
-// result is deterministic.
+// ascending and exactly k long.  Each wavefront compacts a contiguous range of
+// indices, so the workgroup synchronises once for the compaction.  All counts
+// are order independent, so the result is deterministic.
 #include "cs_common.h"
 
 namespace cs {
@@ -74,60 +75,67 @@ __global__ __launch_bounds__(256) void deviation_score_bf16_d128(const Rows rows
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 
-// Block-wide exclusive scan of one flag per thread; returns this thread's
-// rank among set flags and writes the block total to *total.
-__device__ __forceinline__ unsigned block_flag_scan(bool f, unsigned* wsum, unsigned* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const unsigned long long b = __ballot(f);
-  const unsigned lane_rank = __popcll(b & ((1ull << lane) - 1ull));
-  if (lane == 0) wsum[wave] = __popcll(b);
-  __syncthreads();
-  unsigned off = 0, tot = 0;
-#pragma unroll
-  for (int w = 0; w < kSelWaves; ++w) {
-    const unsigned v = wsum[w];
-    off += w < wave ? v : 0u;
-    tot += v;
-  }
-  __syncthreads();
-  *total = tot;
-  return off + lane_rank;
-}
+constexpr int kSelBatch = 8;  // elements per thread (or lane) in flight
 
 __global__ __launch_bounds__(kSelThreads) void radix_select_topk(const float* __restrict__ scores,
                                                                  int n, int k, int cs1,
                                                                  int32_t* __restrict__ sel) {
   __shared__ unsigned hist[kSelWaves][256];
-  __shared__ unsigned tot[256];
+  __shared__ unsigned tot[4];  // per-wavefront totals of the digit scan
   __shared__ unsigned s_prefix, s_kk;
-  __shared__ unsigned wsum[kSelWaves];
+  __shared__ unsigned wgt[kSelWaves], weq[kSelWaves];
   const unsigned* bits = (const unsigned*)scores;
-  const int tid = threadIdx.x, wave = tid >> 6;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   unsigned prefix = 0u, mask = 0u, kk = (unsigned)k;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = tid; b < kSelWaves * 256; b += kSelThreads) (&hist[0][0])[b] = 0u;
     __syncthreads();
-    for (int i = tid; i < n; i += kSelThreads) {
-      const unsigned u = bits[i];
-      if ((u & mask) == prefix) atomicAdd(&hist[wave][(u >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    for (int b = tid; b < 256; b += kSelThreads) {
-      unsigned s = 0;
+    for (int base = tid; base < n; base += kSelBatch * kSelThreads) {
+      unsigned u[kSelBatch];
 #pragma unroll
-      for (int w = 0; w < kSelWaves; ++w) s += hist[w][b];
-      tot[b] = s;
+      for (int j = 0; j < kSelBatch; ++j) {
+        const int i = base + j * kSelThreads;
+        u[j] = i < n ? bits[i] : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < kSelBatch; ++j) {
+        const bool in = base + j * kSelThreads < n && (u[j] & mask) == prefix;
+        const unsigned d = (u[j] >> shift) & 255u;
+        // when every counted lane of the wavefront has the same digit (the
+        // common case in the high digits) one lane adds for all of them
+        const unsigned d0 = __builtin_amdgcn_readfirstlane(d);
+        const unsigned long long act = __ballot(in);
+        if (__ballot(in && d == d0) == act) {
+          if (lane == 0 && act) atomicAdd(&hist[wave][d0], (unsigned)__popcll(act));
+        } else if (in) {
+          atomicAdd(&hist[wave][d], 1u);
+        }
+      }
     }
     __syncthreads();
-    if (tid == 0) {
-      unsigned cum = 0;
-      for (int d = 255; d >= 0; --d) {
-        if (cum + tot[d] >= kk) {
-          s_prefix = prefix | ((unsigned)d << shift);
-          s_kk = kk - cum;
-          break;
-        }
-        cum += tot[d];
+    // Thread b < 256 takes digit d = 255 - b: an inclusive scan over b gives
+    // the count at or above d, and the one digit where that count first
+    // reaches kk is the next digit of the k-th largest pattern.
+    unsigned x = 0, p = 0;
+    if (tid < 256) {
+      const int d = 255 - tid;
+#pragma unroll
+      for (int w = 0; w < kSelWaves; ++w) x += hist[w][d];
+      p = x;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const unsigned y = __shfl_up(p, o);
+        if (lane >= o) p += y;
+      }
+      if (lane == 63) tot[wave] = p;
+    }
+    __syncthreads();
+    if (tid < 256) {
+      for (int w = 0; w < wave; ++w) p += tot[w];
+      const unsigned above = p - x;
+      if (above < kk && kk <= p) {
+        s_prefix = prefix | ((unsigned)(255 - tid) << shift);
+        s_kk = kk - above;
       }
     }
     __syncthreads();
@@ -135,21 +143,59 @@ __global__ __launch_bounds__(kSelThreads) void radix_select_topk(const float* __
     kk = s_kk;
     mask |= 255u << shift;
   }
-  // prefix is now the k-th largest bit pattern; kk ties at it are taken.
+  // prefix is now the k-th largest bit pattern; the first kk ties at it (in
+  // index order) are taken.  Wavefront w compacts the contiguous index range
+  // [w0, w1): a counting pass, one exchange of per-wavefront counts, then a
+  // writing pass in which ballots order the lanes.
   const unsigned thr = prefix;
-  unsigned out_base = 0, eq_base = 0;
-  for (int base = 0; base < n; base += kSelThreads) {
-    const int i = base + tid;
-    const unsigned u = i < n ? bits[i] : 0u;
-    const bool gt = i < n && u > thr;
-    const bool eq = i < n && u == thr;
-    unsigned eq_total, take_total;
-    const unsigned eq_rank = eq_base + block_flag_scan(eq, wsum, &eq_total);
-    const bool take = gt || (eq && eq_rank < kk);
-    const unsigned pos = block_flag_scan(take, wsum, &take_total);
-    if (take && out_base + pos < (unsigned)k) sel[out_base + pos] = cs1 + i;
-    out_base += take_total;
-    eq_base += eq_total;
+  const int per_w = (n + kSelWaves - 1) / kSelWaves;
+  const int w0 = min(n, wave * per_w), w1 = min(n, w0 + per_w);
+  unsigned cgt = 0, ceq = 0;
+  for (int b = w0; b < w1; b += 64 * kSelBatch) {
+    unsigned u[kSelBatch];
+#pragma unroll
+    for (int j = 0; j < kSelBatch; ++j) {
+      const int i = b + 64 * j + lane;
+      u[j] = i < w1 ? bits[i] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kSelBatch; ++j) {
+      const bool ok = b + 64 * j + lane < w1;
+      cgt += (unsigned)__popcll(__ballot(ok && u[j] > thr));
+      ceq += (unsigned)__popcll(__ballot(ok && u[j] == thr));
+    }
+  }
+  if (lane == 0) {
+    wgt[wave] = cgt;
+    weq[wave] = ceq;
+  }
+  __syncthreads();
+  unsigned eq_run = 0, out_run = 0;  // ties and outputs before this wavefront's range
+  for (int v = 0; v < wave; ++v) {
+    out_run += wgt[v] + min(weq[v], kk > eq_run ? kk - eq_run : 0u);
+    eq_run += weq[v];
+  }
+  const unsigned long long below = (1ull << lane) - 1ull;
+  for (int b = w0; b < w1; b += 64 * kSelBatch) {
+    unsigned u[kSelBatch];
+#pragma unroll
+    for (int j = 0; j < kSelBatch; ++j) {
+      const int i = b + 64 * j + lane;
+      u[j] = i < w1 ? bits[i] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kSelBatch; ++j) {
+      const int i = b + 64 * j + lane;
+      const bool ok = i < w1;
+      const bool eq = ok && u[j] == thr;
+      const unsigned long long em = __ballot(eq);
+      const bool take = (ok && u[j] > thr) || (eq && eq_run + (unsigned)__popcll(em & below) < kk);
+      const unsigned long long tm = __ballot(take);
+      const unsigned pos = out_run + (unsigned)__popcll(tm & below);
+      if (take && pos < (unsigned)k) sel[pos] = cs1 + i;
+      out_run += (unsigned)__popcll(tm);
+      eq_run += (unsigned)__popcll(em);
+    }
   }
 }
 

@@ -219,6 +219,39 @@ def test_qwen8k_score_select_isolated(qwen8k):
     assert sel[:k].cpu().numpy().tolist() == oracle.select.select_top(ref_scores, k, w.cs1).tolist()
 
 
+@pytest.mark.parametrize("n_tok,seed", [(3000, 5), (70000, 6)])
+def test_select_heavy_ties(n_tok, seed):
+    """Scores from the four values 0, 1, 2, 3 (exactly): every threshold falls
+    inside a tie group, so the selection must take the lowest indices of that
+    group, across the ranges of several wavefronts."""
+    w = ragged(n_layers=1, chunk_lens=(64, n_tok - 64), offsets="none")
+    log(f"case select ties n={n_tok}")
+    b = B()
+    geo = b.Geo.from_workload(w)
+    rng = np.random.default_rng(seed)
+    H, T, D, cs1 = w.n_kv_heads, w.n_tokens, w.head_dim, w.cs1
+    k_cache = obf.encode(rng.standard_normal((1, H, T, D)))
+    k_cache[..., 0] = obf.encode(np.zeros(1))[0]
+    kf = k_cache[0][:, cs1:].copy()
+    v = rng.integers(0, 4, size=T - cs1)
+    kf[0, :, 0] = obf.encode(v.astype(np.float64))
+    ref = oracle.score.deviation_f32(dec(k_cache[0], w.dtype), dec(kf, w.dtype), cs1)
+    assert np.array_equal(ref, v.astype(np.float32))   # delta_t = v_t exactly
+    K, KF = to_dev(k_cache, w.dtype), to_dev(kf, w.dtype)
+    n = T - cs1
+    for rho in (1e-9, 0.1, 0.25, 0.26, 0.5, 0.77, 1.0):
+        sel = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+        scores = torch.empty(n, dtype=torch.float32, device="cuda")
+        k = b.score_deviation_topk(geo, K, 0, KF, rho, scores, sel)
+        torch.cuda.synchronize()
+        assert np.array_equal(scores.cpu().numpy(), ref)
+        want = oracle.select.select_top(ref, oracle.select.n_select(rho, n), cs1)
+        got = sel.cpu().numpy()
+        assert k == len(want)
+        assert got[:k].tolist() == want.tolist()
+        assert (got[k:] == -1).all()
+
+
 def test_qwen8k_attention_isolated(qwen8k):
     w, d, k_reb = qwen8k
     ref_scores = oracle.score.deviation_f32(dec(k_reb[w.score_layer], w.dtype),
