@@ -9,9 +9,11 @@
 // largest bit pattern by a 4-pass, 8-bit MSB-first radix select with LDS
 // histograms, then compacts in index order: every score above the threshold
 // and the first (lowest-index) ties at the threshold, so the output is
-// ascending and exactly k long.  Each wavefront compacts a contiguous range of
-// indices, so the workgroup synchronises once for the compaction.  All counts
-// are order independent, so the result is deterministic.
+// ascending and exactly k long.  Up to 65,536 candidates the scores are read
+// once into registers (64 per thread, a contiguous range each) and the
+// compaction takes two workgroup scans; beyond that every pass re-reads them
+// and each wavefront compacts a contiguous range.  All counts are order
+// independent, so the result is deterministic.
 #include "cs_common.h"
 
 namespace cs {
@@ -75,8 +77,15 @@ __global__ __launch_bounds__(256) void deviation_score_bf16_d128(const Rows rows
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 
-constexpr int kSelBatch = 8;  // elements per thread (or lane) in flight
+constexpr int kSelBatch = 8;   // elements per thread (or lane) in flight
+constexpr int kSelHeld = 64;   // elements a thread keeps in registers (n <= kSelHeld x kSelThreads)
 
+// kHeld: n <= kSelHeld x kSelThreads, and wavefront w keeps the scores
+// [64 kSelHeld w, 64 kSelHeld (w + 1)) in registers for all passes (lane l
+// holds index 64 kSelHeld w + 64 j + l as its j-th value, so every load is
+// coalesced); otherwise every pass re-reads the scores.  Either way each
+// wavefront then compacts a contiguous range of indices.
+template <bool kHeld>
 __global__ __launch_bounds__(kSelThreads) void radix_select_topk(const float* __restrict__ scores,
                                                                  int n, int k, int cs1,
                                                                  int32_t* __restrict__ sel) {
@@ -86,30 +95,49 @@ __global__ __launch_bounds__(kSelThreads) void radix_select_topk(const float* __
   __shared__ unsigned wgt[kSelWaves], weq[kSelWaves];
   const unsigned* bits = (const unsigned*)scores;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  // held slots past n carry 0xffffffff, a pattern with the sign bit set that
+  // no score (all are >= 0) has, so it matches no prefix and is never above
+  // or at the threshold (compared as signed integers)
+  const int hb = 64 * kSelHeld * wave;  // first index this wavefront holds
+  unsigned held[kHeld ? kSelHeld : 1];
+  if constexpr (kHeld) {
+#pragma unroll
+    for (int j = 0; j < kSelHeld; ++j) {
+      const int i = hb + 64 * j + lane;
+      held[j] = i < n ? bits[i] : 0xffffffffu;
+    }
+  }
+  // adds one element to this wavefront's histogram; when every counted lane
+  // of the wavefront has the same digit (the common case in the high digits)
+  // one lane adds for all of them
+  auto count = [&](bool in, unsigned d) {
+    const unsigned d0 = __builtin_amdgcn_readfirstlane(d);
+    const unsigned long long act = __ballot(in);
+    if (__ballot(in && d == d0) == act) {
+      if (lane == __builtin_amdgcn_readfirstlane(lane) && act) atomicAdd(&hist[wave][d0], (unsigned)__popcll(act));
+    } else if (in) {
+      atomicAdd(&hist[wave][d], 1u);
+    }
+  };
   unsigned prefix = 0u, mask = 0u, kk = (unsigned)k;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = tid; b < kSelWaves * 256; b += kSelThreads) (&hist[0][0])[b] = 0u;
     __syncthreads();
-    for (int base = tid; base < n; base += kSelBatch * kSelThreads) {
-      unsigned u[kSelBatch];
+    if constexpr (kHeld) {
 #pragma unroll
-      for (int j = 0; j < kSelBatch; ++j) {
-        const int i = base + j * kSelThreads;
-        u[j] = i < n ? bits[i] : 0u;
-      }
+      for (int j = 0; j < kSelHeld; ++j)
+        if ((held[j] & (mask | 0x80000000u)) == prefix) atomicAdd(&hist[wave][(held[j] >> shift) & 255u], 1u);
+    } else {
+      for (int base = tid; base < n; base += kSelBatch * kSelThreads) {
+        unsigned u[kSelBatch];
 #pragma unroll
-      for (int j = 0; j < kSelBatch; ++j) {
-        const bool in = base + j * kSelThreads < n && (u[j] & mask) == prefix;
-        const unsigned d = (u[j] >> shift) & 255u;
-        // when every counted lane of the wavefront has the same digit (the
-        // common case in the high digits) one lane adds for all of them
-        const unsigned d0 = __builtin_amdgcn_readfirstlane(d);
-        const unsigned long long act = __ballot(in);
-        if (__ballot(in && d == d0) == act) {
-          if (lane == 0 && act) atomicAdd(&hist[wave][d0], (unsigned)__popcll(act));
-        } else if (in) {
-          atomicAdd(&hist[wave][d], 1u);
+        for (int j = 0; j < kSelBatch; ++j) {
+          const int i = base + j * kSelThreads;
+          u[j] = i < n ? bits[i] : 0u;
         }
+#pragma unroll
+        for (int j = 0; j < kSelBatch; ++j)
+          count(base + j * kSelThreads < n && (u[j] & mask) == prefix, (u[j] >> shift) & 255u);
       }
     }
     __syncthreads();
@@ -144,57 +172,94 @@ __global__ __launch_bounds__(kSelThreads) void radix_select_topk(const float* __
     mask |= 255u << shift;
   }
   // prefix is now the k-th largest bit pattern; the first kk ties at it (in
-  // index order) are taken.  Wavefront w compacts the contiguous index range
-  // [w0, w1): a counting pass, one exchange of per-wavefront counts, then a
-  // writing pass in which ballots order the lanes.
+  // index order) are taken.
   const unsigned thr = prefix;
-  const int per_w = (n + kSelWaves - 1) / kSelWaves;
-  const int w0 = min(n, wave * per_w), w1 = min(n, w0 + per_w);
-  unsigned cgt = 0, ceq = 0;
-  for (int b = w0; b < w1; b += 64 * kSelBatch) {
-    unsigned u[kSelBatch];
-#pragma unroll
-    for (int j = 0; j < kSelBatch; ++j) {
-      const int i = b + 64 * j + lane;
-      u[j] = i < w1 ? bits[i] : 0u;
-    }
-#pragma unroll
-    for (int j = 0; j < kSelBatch; ++j) {
-      const bool ok = b + 64 * j + lane < w1;
-      cgt += (unsigned)__popcll(__ballot(ok && u[j] > thr));
-      ceq += (unsigned)__popcll(__ballot(ok && u[j] == thr));
-    }
-  }
-  if (lane == 0) {
-    wgt[wave] = cgt;
-    weq[wave] = ceq;
-  }
-  __syncthreads();
-  unsigned eq_run = 0, out_run = 0;  // ties and outputs before this wavefront's range
-  for (int v = 0; v < wave; ++v) {
-    out_run += wgt[v] + min(weq[v], kk > eq_run ? kk - eq_run : 0u);
-    eq_run += weq[v];
-  }
   const unsigned long long below = (1ull << lane) - 1ull;
-  for (int b = w0; b < w1; b += 64 * kSelBatch) {
-    unsigned u[kSelBatch];
+  if constexpr (kHeld) {
+    // the held values in index order: j, then lane
+    unsigned cgt = 0, ceq = 0;
 #pragma unroll
-    for (int j = 0; j < kSelBatch; ++j) {
-      const int i = b + 64 * j + lane;
-      u[j] = i < w1 ? bits[i] : 0u;
+    for (int j = 0; j < kSelHeld; ++j) {
+      cgt += (int)held[j] > (int)thr;
+      ceq += held[j] == thr;
     }
 #pragma unroll
-    for (int j = 0; j < kSelBatch; ++j) {
-      const int i = b + 64 * j + lane;
-      const bool ok = i < w1;
-      const bool eq = ok && u[j] == thr;
+    for (int o = 32; o; o >>= 1) {
+      cgt += __shfl_xor(cgt, o);
+      ceq += __shfl_xor(ceq, o);
+    }
+    if (lane == 0) {
+      wgt[wave] = cgt;
+      weq[wave] = ceq;
+    }
+    __syncthreads();
+    unsigned eq_run = 0, out_run = 0;  // ties and outputs before this wavefront's range
+    for (int v = 0; v < wave; ++v) {
+      out_run += wgt[v] + min(weq[v], kk > eq_run ? kk - eq_run : 0u);
+      eq_run += weq[v];
+    }
+#pragma unroll
+    for (int j = 0; j < kSelHeld; ++j) {
+      const bool eq = held[j] == thr;
       const unsigned long long em = __ballot(eq);
-      const bool take = (ok && u[j] > thr) || (eq && eq_run + (unsigned)__popcll(em & below) < kk);
+      const bool take = (int)held[j] > (int)thr || (eq && eq_run + (unsigned)__popcll(em & below) < kk);
       const unsigned long long tm = __ballot(take);
       const unsigned pos = out_run + (unsigned)__popcll(tm & below);
-      if (take && pos < (unsigned)k) sel[pos] = cs1 + i;
+      if (take && pos < (unsigned)k) sel[pos] = cs1 + hb + 64 * j + lane;
       out_run += (unsigned)__popcll(tm);
       eq_run += (unsigned)__popcll(em);
+    }
+  } else {
+    // Wavefront w compacts the contiguous index range [w0, w1): a counting
+    // pass, one exchange of per-wavefront counts, then a writing pass in
+    // which ballots order the lanes.
+    const int per_w = (n + kSelWaves - 1) / kSelWaves;
+    const int w0 = min(n, wave * per_w), w1 = min(n, w0 + per_w);
+    unsigned cgt = 0, ceq = 0;
+    for (int b = w0; b < w1; b += 64 * kSelBatch) {
+      unsigned u[kSelBatch];
+#pragma unroll
+      for (int j = 0; j < kSelBatch; ++j) {
+        const int i = b + 64 * j + lane;
+        u[j] = i < w1 ? bits[i] : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < kSelBatch; ++j) {
+        const bool ok = b + 64 * j + lane < w1;
+        cgt += (unsigned)__popcll(__ballot(ok && u[j] > thr));
+        ceq += (unsigned)__popcll(__ballot(ok && u[j] == thr));
+      }
+    }
+    if (lane == 0) {
+      wgt[wave] = cgt;
+      weq[wave] = ceq;
+    }
+    __syncthreads();
+    unsigned eq_run = 0, out_run = 0;  // ties and outputs before this wavefront's range
+    for (int v = 0; v < wave; ++v) {
+      out_run += wgt[v] + min(weq[v], kk > eq_run ? kk - eq_run : 0u);
+      eq_run += weq[v];
+    }
+    for (int b = w0; b < w1; b += 64 * kSelBatch) {
+      unsigned u[kSelBatch];
+#pragma unroll
+      for (int j = 0; j < kSelBatch; ++j) {
+        const int i = b + 64 * j + lane;
+        u[j] = i < w1 ? bits[i] : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < kSelBatch; ++j) {
+        const int i = b + 64 * j + lane;
+        const bool ok = i < w1;
+        const bool eq = ok && u[j] == thr;
+        const unsigned long long em = __ballot(eq);
+        const bool take = (ok && u[j] > thr) || (eq && eq_run + (unsigned)__popcll(em & below) < kk);
+        const unsigned long long tm = __ballot(take);
+        const unsigned pos = out_run + (unsigned)__popcll(tm & below);
+        if (take && pos < (unsigned)k) sel[pos] = cs1 + i;
+        out_run += (unsigned)__popcll(tm);
+        eq_run += (unsigned)__popcll(em);
+      }
     }
   }
 }
@@ -230,8 +295,12 @@ cs_status launch_score_select(const Geo& g, const CacheView& cv, int score_layer
   if (st || k_sel == 0) return st;
   {
     TraceScope tr("radix_select_topk", s);
-    hipLaunchKernelGGL(radix_select_topk, dim3(1), dim3(kSelThreads), 0, s, scores, (int)g.n, (int)k_sel,
-                       (int)g.cs1, sel);
+    if (g.n <= (int64_t)kSelHeld * kSelThreads)
+      hipLaunchKernelGGL(radix_select_topk<true>, dim3(1), dim3(kSelThreads), 0, s, scores, (int)g.n, (int)k_sel,
+                         (int)g.cs1, sel);
+    else
+      hipLaunchKernelGGL(radix_select_topk<false>, dim3(1), dim3(kSelThreads), 0, s, scores, (int)g.n,
+                         (int)k_sel, (int)g.cs1, sel);
   }
   return check_launch("top-k select launch");
 }
