@@ -543,6 +543,15 @@ def test_more_than_1024_row_tiles():
     _isolated_full_size(w, rhos=(1.0,), n_random=64, check_rebase=False)
 
 
+def test_more_than_4096_row_tiles():
+    """34,000 selected rows at G = 32 make 4,250 row tiles: more than the
+    planning workgroup keeps in LDS, so the plan reads its arrays back from
+    global memory (with this many row tiles the even schedule cuts none)."""
+    w = ragged(n_layers=1, G=32, Hkv=1, chunk_lens=(64, 34000))
+    log(f"case ragged G=32 Hkv=1 lens=(64, 34000) rho=1")
+    _isolated_full_size(w, rhos=(1.0,), n_random=48, check_rebase=False)
+
+
 # ======================================================================== per-token rebase (Section 3 policies)
 def _gpu_rebase_tokens(w, k_stored, toff):
     b = B()
