@@ -218,6 +218,7 @@ constexpr int kMinPiece = 64;   // smallest piece: 64 key tiles (an item's fixed
 constexpr int kPartCap = 2560;  // partial slots per layer, at most
 constexpr int kPlanLdsTiles = 4096;  // row tiles whose plan arrays the planning workgroup keeps in LDS
 constexpr int kPlanLdsPieces = 2049; // most pieces of a row tile (T < 2^23: ceil(ceil(T / 64) / kMinPiece) <= 2048), + 1
+constexpr int kPlanSortCap = 2048;   // longest tail (a quarter of a queue) the plan reorders
 constexpr int kXcds = 8;
 
 struct PlanView {
@@ -397,23 +398,68 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   // Item descriptors, one per queue position (the same in every queue and
   // layer): {row tile, KV head in the queue | piece << 16, first and last key
   // tile of the piece}.  Cut row tiles are a prefix of the longest-first order,
-  // so piece j of row tile i sits at pj[j] + kvl * cnt_j + i.
+  // so piece j of row tile i sits at pj[j] + kvl * cnt_j + i.  The last
+  // quarter of the queue (the part handed out by the atomic counters) is
+  // reordered longest first, so the launch ends on its shortest items; the
+  // order of equal lengths is immaterial (an item's descriptor alone fixes
+  // its work and its output slots).
+  __shared__ int4 l_desc[kPlanSortCap];
+  __shared__ int l_bkt[256];
+  if (tid < 256) l_bkt[tid] = 0;
   __syncthreads();
   int4* desc = (int4*)(plan + desc_off);
   const int p_end = l_pj[nj];
   const int nun = (int)(n_tiles - n_cut);
+  const int per_q_all = s_base + nun * kvq;
+  const int r0 = per_q_all - (per_q_all + 3) / 4;
+  const bool sort_tail = per_q_all - r0 <= kPlanSortCap;
+  auto put = [&](int pos, int4 d) {
+    if (sort_tail && pos >= r0) l_desc[pos - r0] = d;
+    else desc[pos] = d;
+  };
   for (int64_t i = tid; i < n_tiles; i += 1024) {
     const int v = nu[i], np = nsp[i];
     if (np > 1) {
       for (int j = 0; j < np; ++j) {
         const int cnt = (l_pj[j + 1] - l_pj[j]) / kvq;
         const int b = (int)((int64_t)j * v / np), e = (int)((int64_t)(j + 1) * v / np);
-        for (int kvl = 0; kvl < kvq; ++kvl) desc[l_pj[j] + kvl * cnt + i] = make_int4((int)i, kvl | (j << 16), b, e);
+        for (int kvl = 0; kvl < kvq; ++kvl) put(l_pj[j] + kvl * cnt + (int)i, make_int4((int)i, kvl | (j << 16), b, e));
       }
     } else {
-      for (int kvl = 0; kvl < kvq; ++kvl)
-        desc[p_end + kvl * nun + (int)(i - n_cut)] = make_int4((int)i, kvl, 0, v);
+      for (int kvl = 0; kvl < kvq; ++kvl) put(p_end + kvl * nun + (int)(i - n_cut), make_int4((int)i, kvl, 0, v));
     }
+  }
+  if (!sort_tail) return;  // (uniform)
+  // counting sort of the tail by length (at most S key tiles), longest first,
+  // in 256 buckets
+  __syncthreads();
+  const int nt = per_q_all - r0;
+  int shift = 0;
+  while ((S >> shift) > 255) ++shift;
+  auto bucket = [&](int4 d) { return 255 - min((d.w - d.z) >> shift, 255); };
+  for (int t = tid; t < nt; t += 1024) atomicAdd(&l_bkt[bucket(l_desc[t])], 1);
+  __syncthreads();
+  if (tid < 64) {  // exclusive scan of the 256 bucket counts by one wavefront
+    int c4[4], tot = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tot += c4[q] = l_bkt[4 * tid + q];
+    int incl = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (tid >= o) incl += y;
+    }
+    int run = incl - tot;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      l_bkt[4 * tid + q] = run;
+      run += c4[q];
+    }
+  }
+  __syncthreads();
+  for (int t = tid; t < nt; t += 1024) {
+    const int4 d = l_desc[t];
+    desc[r0 + atomicAdd(&l_bkt[bucket(d)], 1)] = d;
   }
 }
 
