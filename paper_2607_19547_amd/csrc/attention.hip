@@ -557,38 +557,20 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
 
   const int lrel = item / per_q;
   const int r = item - lrel * per_q;
-  const int4 dsc = *(const int4*)(a.plan + pv.hdr[14] + 4 * r);  // the item's descriptor
+  const int4 dsc = *(const int4*)(a.plan + a.desc_off + 4 * r);  // the item's descriptor
   const int oi = dsc.x, kvl = dsc.y & 0xffff, piece = dsc.y >> 16;
   const int64_t seg_b = dsc.z, seg_e = dsc.w;
-  const int nsp = pv.nsp[oi];  // for the epilogue
   const int kv = kvl * nq + jq;
-  const bool full = nsp == 1;
   const int64_t tile = a.n_tiles - 1 - oi;
   const int layer = a.lb + lrel;
-
-  const int64_t m0 = tile * RT;
-  const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
-  const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
   const int key_begin = (int)(seg_b * kKT);
-  const int key_end = min((int)(seg_e * kKT), g_last + 1);
 
-  const int64_t m = m0 + wave * RW + q / G;
-  const int h = kv * G + q % G;
-  int g_q = -1;
-  if (m < a.n_sel) {
-    const int t = a.sel[m];
-    if (t >= a.cs1 && t < a.T) g_q = t;
-  }
-  const bool valid = g_q >= 0;
-  const int64_t mw0 = m0 + wave * RW;
-  const int64_t mw1 = min(mw0 + RW, a.n_sel) - 1;
-  const int g_wmin = mw0 < a.n_sel ? a.sel[mw0] : 0x7fffffff;
-  const int g_wmax = mw0 < a.n_sel ? a.sel[mw1] : -1;
-
-  // Key tiles are fetched in ascending order.  A contiguous cache is one
-  // buffer range per plane; in a paged cache every 64-key tile lies inside
-  // one chunk (chunk starts are multiples of 64), and the range follows the
-  // chunk of the tile being fetched.  Rows past a range read as zeros.
+  // Key tiles are fetched in ascending order, the first three as soon as the
+  // descriptor is known (the item's remaining loads overlap them).  A
+  // contiguous cache is one buffer range per plane; in a paged cache every
+  // 64-key tile lies inside one chunk (chunk starts are multiples of 64), and
+  // the range follows the chunk of the tile being fetched.  Rows past a range
+  // read as zeros.
   const int64_t plane = (int64_t)layer * a.Hkv + kv;
   __amdgpu_buffer_rsrc_t rk, rv;
   int dma_c = 0, dma_first = 0, dma_next = 0x7fffffff;
@@ -618,10 +600,30 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     }
     stage_dma(rk, rv, so, kt - dma_first, Kd, Vd, wave);
   };
-  const int n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
   fetch(key_begin, up_k0, lo_v0);
   fetch(key_begin + kKT, up_k1, lo_v1);
   fetch(key_begin + 2 * kKT, up_k2, lo_v2);
+
+  const int nsp = pv.nsp[oi];  // for the epilogue
+  const bool full = nsp == 1;
+  const int64_t m0 = tile * RT;
+  const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
+  const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
+  const int key_end = min((int)(seg_e * kKT), g_last + 1);
+  const int n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
+
+  const int64_t m = m0 + wave * RW + q / G;
+  const int h = kv * G + q % G;
+  int g_q = -1;
+  if (m < a.n_sel) {
+    const int t = a.sel[m];
+    if (t >= a.cs1 && t < a.T) g_q = t;
+  }
+  const bool valid = g_q >= 0;
+  const int64_t mw0 = m0 + wave * RW;
+  const int64_t mw1 = min(mw0 + RW, a.n_sel) - 1;
+  const int g_wmin = mw0 < a.n_sel ? a.sel[mw0] : 0x7fffffff;
+  const int g_wmax = mw0 < a.n_sel ? a.sel[mw1] : -1;
 
   bf16x8 qb[8];
   if (valid) {
