@@ -145,3 +145,25 @@ def test_layer0_fidelity_ordering_table1():
     assert rel_mse(three) < 1e-4          # bf16 rounding level (two roundings)
     assert rel_mse(naive) > 1e-2
     assert rel_mse(three) < rel_mse(naive) * 1e-2
+
+
+def test_float32_angles_fail_at_large_offsets():
+    """P2: why the delta angles are formed in float64.  At Delta_t = 1e5 the
+    temporal pairs turn by up to 1e5 rad, where float32 spacing is 2^-7 rad;
+    forming Delta_t * theta_i in float32 moves the rotated key by more than a
+    bf16 ulp, while the float64 angles of the oracle keep the single rounding."""
+    th, sg = rope.inv_freq(128, 1e6), rope.axis_of_pair((16, 24, 24))
+    rng = np.random.default_rng(21)
+    x = bf16.decode(bf16.encode(rng.standard_normal((4096, 128))))
+    off = np.array([[100000, 0, 0]])
+    exact_phi = rebase.chunk_phases(off, th, sg)[0]
+    phi32 = (np.float32(off[0, 0]) * th.astype(np.float32)).astype(np.float64)
+    phi32 = np.where(sg == 0, phi32, exact_phi)          # only the temporal pairs move
+    exact = rope.rotate_pairs(x, exact_phi)
+    via32 = bf16.decode(bf16.encode(rope.rotate_pairs(x, phi32)))
+    via64 = bf16.decode(rebase.rebase_stored(bf16.encode(x), "bf16", np.array([0, 4096]), off, th, sg))
+    _, e = np.frexp(np.abs(exact))
+    ulp = np.ldexp(1.0, np.maximum(e - 1, -126) - 7)    # bf16 spacing at each exact value
+    assert np.max(np.abs(via32 - exact) / ulp) > 1.0    # float32 angles: beyond one bf16 ulp
+    assert np.all(np.abs(via64 - exact) <= 0.5 * ulp)   # float64 angles: one correct rounding
+    assert np.array_equal(via64, bf16.decode(bf16.encode(exact)))
