@@ -403,6 +403,40 @@ def test_rebase_large_offsets_all_axes():
     assert rel < 2e-5
 
 
+def test_rebase_extreme_offsets():
+    """Offsets of up to 2^30 on every axis (the temporal pairs turn by up to
+    1.07e9 rad): the per-chunk and per-token kernels reduce the float64 angle
+    on both sides of the Cody-Waite range (|k| < 2^27 turns) and stay within
+    one rounding of the oracle's exact rotation."""
+    w = ragged(n_layers=2, chunk_lens=(64, 128, 192, 256, 100), offsets="none")
+    th, sg = theta_sigma(w)
+    off = np.array([[0, 0, 0],
+                    [1 << 30, -(1 << 30), 123456789],
+                    [-(1 << 30) + 7, 1 << 29, -(1 << 29) - 3],
+                    [800000000, -800000001, 799999999],     # just inside |k| < 2^27 for theta_0 = 1
+                    [-850000000, 2147483, -17]], dtype=np.int32)
+    log(f"case rebase extreme offsets {off.tolist()}")
+    rng = np.random.default_rng(13)
+    stored = obf.encode(rng.standard_normal((w.n_layers, w.n_kv_heads, w.n_tokens, w.head_dim)))
+    want = oracle.rebase.rebase_stored(stored, w.dtype, w.chunk_start, off, th, sg)
+    b = B()
+    geo = b.Geo.from_workload(w)
+    K = to_dev(stored, w.dtype)
+    b.compose_rebase_k(geo, K, off)
+    torch.cuda.synchronize()
+    got = to_host(K, w.dtype)
+    g, o = dec(got, w.dtype), dec(want, w.dtype)
+    assert np.all(np.abs(g - o) <= ulp(o, w.dtype) + 2.0 ** -20 * pair_norm(o))
+    c1 = int(w.chunk_start[1])
+    assert np.array_equal(got[:, :, :c1], stored[:, :, :c1])      # chunk 0 has Delta = 0
+    log(f"  {int((got != want).sum())} of {want.size} elements differ by one rounding")
+    toff = np.repeat(off, np.diff(w.chunk_start), axis=0)
+    K2 = to_dev(stored, w.dtype)
+    b.compose_rebase_k_tokens(geo, K2, torch.from_numpy(np.ascontiguousarray(toff)).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(K2, w.dtype), to_host(K, w.dtype))
+
+
 def test_workspace_reuse_and_garbage_workspace():
     """Partial results of cut row tiles live in the caller's workspace: a workspace full of
     garbage must work, and repeated calls on one workspace must give
