@@ -359,6 +359,25 @@ def test_ragged_geometries(G, Hkv, lens, rho):
     assert np.array_equal(out2, out) and np.array_equal(kp2, kp)
 
 
+def _random_geometries(n=10, seed=2026):
+    """Seeded draws of GQA group, KV heads, chunk lengths (1-399 tokens, 2-6
+    chunks) and rho, beyond the hand-picked cases above."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        G = (1, 2, 4, 8, 16, 32)[i % 6]
+        Hkv = int(rng.choice([1, 2, 3, 4])) if G <= 8 else int(rng.choice([1, 2]))
+        lens = tuple(int(x) for x in rng.integers(1, 400, int(rng.integers(2, 7))))
+        rho = float(np.round(rng.uniform(0.02, 1.0), 3))
+        cases.append((G, Hkv, lens, rho))
+    return cases
+
+
+@pytest.mark.parametrize("G,Hkv,lens,rho", _random_geometries())
+def test_random_geometries(G, Hkv, lens, rho):
+    test_ragged_geometries(G, Hkv, lens, rho)
+
+
 def test_rho_zero_and_single_chunk():
     w = ragged(chunk_lens=(100, 130, 103, 167))
     d = oracle.inputs.build(w)
