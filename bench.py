@@ -450,7 +450,14 @@ def cpu_baseline(w, rho):
         threads = os.cpu_count()
     log(f"[bench] cpu_baseline: rebase/layer {t_rebase:.2f} s, score+select {t_select:.2f} s, "
         f"attention/layer {t_attn:.2f} s -> {total_s:.1f} s per composition (extrapolated)")
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
     return dict(value=total_s * 1e3, unit="ms", cores=threads, kind="oracle",
+                host_cpus=os.cpu_count(), cpu_model=cpu_model,
                 sample=(f"1 of {w.n_layers} layers (rebase {t_rebase:.2f} s + scatter/attention "
                         f"{t_attn:.2f} s, measured) x {w.n_layers} + score/select {t_select:.2f} s "
                         f"(measured, full); float64 numpy on the host"))
