@@ -129,6 +129,25 @@ def test_paged_compose_equals_contiguous(lens, G, Hkv, rho, kind):
     assert np.array_equal(paged2["out"], paged["out"]) and np.array_equal(flat2["out"], paged["out"])
 
 
+def _random_paged(n=6, seed=77):
+    """Seeded paged geometries for the MFMA path: 2-12 chunks of 64-1024 tokens
+    in whole 64-token tiles, a ragged last chunk, every GQA group."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        G = (1, 2, 4, 8, 16, 32)[i % 6]
+        Hkv = int(rng.choice([1, 2, 4])) if G <= 8 else 1
+        nch = int(rng.integers(2, 13))
+        lens = [64 * int(x) for x in rng.integers(1, 17, nch - 1)] + [int(rng.integers(1, 700))]
+        cases.append((tuple(lens), G, Hkv, float(np.round(rng.uniform(0.02, 1.0), 3)), "bf16"))
+    return cases
+
+
+@pytest.mark.parametrize("lens,G,Hkv,rho,kind", _random_paged())
+def test_paged_random_equals_contiguous(lens, G, Hkv, rho, kind):
+    test_paged_compose_equals_contiguous(lens, G, Hkv, rho, kind)
+
+
 @pytest.mark.parametrize("lens,G,Hkv,rho,kind", CASES[:2] + CASES[4:])
 def test_paged_isolated_against_oracle(lens, G, Hkv, rho, kind):
     """Each paged stage from the oracle's inputs, against the oracle."""
