@@ -208,9 +208,10 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_bu
 // Within a queue, the pieces of cut row tiles come first,
 // piece-major (piece 0 of every cut row tile, then piece 1, ...: workgroups
 // running side by side read the same keys), then the uncut row tiles, longest
-// first, so each XCD ends with its smallest items.  The pieces of a cut row
-// tile leave partial (O, max, sum) in fixed workspace slots that
-// sel_attn_combine merges in piece order.
+// first; the counter-dealt last quarter is then reordered longest first, so a
+// launch ends on its shortest items.  The pieces of a cut row tile leave
+// partial (O, max, sum) in fixed workspace slots that sel_attn_combine merges
+// in piece order.
 constexpr int kPlanHdr = 16;    // header ints, see PlanView
 constexpr int kPlanCUs = 256;   // CU count S is derived from (a constant: results do not depend on the device)
 constexpr int kItemsPerCU = 6;  // target items per CU when row tiles must be cut
