@@ -227,7 +227,14 @@ cs_status selective_attend_scatter_rope(const cs_geometry* g, void* k_cache,
  *   k_cache,v_cache DEVICE [L][H_kv][T][D], rows sel_idx overwritten in place
  *   layer_begin, layer_end  0 <= begin <= end <= L
  *   sel_idx        DEVICE int32 [n_sel], strictly ascending, in [s_1, T)
- *                  (as written by score_deviation_topk; not checked)
+ *                  (as written by score_deviation_topk).  Not checked unless
+ *                  the environment variable CS_DEBUG_VALIDATE is "1": then a
+ *                  violation returns CS_ERR_INVALID_ARGUMENT before anything
+ *                  else is enqueued, at the cost of a synchronisation of the
+ *                  stream (a debugging aid; such calls must not overlap on one
+ *                  GPU).  Unchecked, an index outside [s_1, T) is skipped and
+ *                  an unsorted list gives wrong outputs, never an access
+ *                  outside the caller's buffers.
  *   n_sel          0 <= n_sel <= n
  *   q_fresh        DEVICE [L][H_q][n][D] fresh queries (post-rotary, global)
  *   k_fresh,v_fresh DEVICE [L][H_kv][n][D] fresh keys / values

@@ -1,6 +1,7 @@
 // C-ABI entry points: argument validation, host-side coordinate shift,
 // workspace sizing, kernel tracing and error reporting.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <map>
@@ -228,6 +229,49 @@ static cs_status score_topk(const Geo& g, const CacheView& cv, int32_t score_lay
   return launch_score_select(g, cv, score_layer, k_fresh, scores, sel_idx, k, (hipStream_t)stream);
 }
 
+// ------------------------------------------------------------------ debug validation
+// With the environment variable CS_DEBUG_VALIDATE=1 the attention entry points
+// check the selection's unchecked precondition on the device (strictly
+// ascending, every index in [s_1, T)) before enqueuing anything else, at the
+// cost of a synchronisation of the stream.  The violation flag is one word of
+// device memory per GPU, so validated calls must not overlap.
+static __device__ unsigned g_sel_bad;
+
+__global__ __launch_bounds__(256) void validate_sel(const int32_t* __restrict__ sel, int64_t n_sel, int64_t lo,
+                                                    int64_t hi) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_sel) return;
+  const int64_t v = sel[i];
+  unsigned bad = 0;
+  if (v < lo || v >= hi) bad |= 1u;
+  if (i > 0 && (int64_t)sel[i - 1] >= v) bad |= 2u;
+  if (bad) atomicOr(&g_sel_bad, bad);
+}
+
+static bool debug_validate() {
+  const char* e = getenv("CS_DEBUG_VALIDATE");
+  return e && e[0] == '1' && e[1] == 0;
+}
+
+static cs_status check_selection(const Geo& g, const int32_t* sel, int64_t n_sel, hipStream_t s) {
+  if (n_sel <= 0) return CS_OK;
+  const int64_t blocks = (n_sel + 255) / 256;
+  cs_status st = check_grid(blocks, 1, 1, 256, "selection check");
+  if (st) return st;
+  unsigned flag = 0;
+  if (hipMemcpyToSymbolAsync(HIP_SYMBOL(g_sel_bad), &flag, sizeof flag, 0, hipMemcpyHostToDevice, s) != hipSuccess)
+    return fail(CS_ERR_HIP, "selection check: clearing the flag failed");
+  hipLaunchKernelGGL(validate_sel, dim3((unsigned)blocks), dim3(256), 0, s, sel, n_sel, g.cs1, g.T);
+  st = check_launch("selection check launch");
+  if (st) return st;
+  if (hipMemcpyFromSymbolAsync(&flag, HIP_SYMBOL(g_sel_bad), sizeof flag, 0, hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(CS_ERR_HIP, "selection check: reading the flag failed");
+  if (flag & 1u) return fail(CS_ERR_INVALID_ARGUMENT, "sel_idx holds an index outside [chunk_start[1], n_tokens)");
+  if (flag & 2u) return fail(CS_ERR_INVALID_ARGUMENT, "sel_idx is not strictly ascending");
+  return CS_OK;
+}
+
 static cs_status attend_scatter(const Geo& g, const CacheView& cv, int32_t layer_begin, int32_t layer_end,
                                 const int32_t* sel_idx, int64_t n_sel, const void* q_fresh, const void* k_fresh,
                                 const void* v_fresh, void* out, float* lse, void* workspace, size_t workspace_bytes,
@@ -246,6 +290,10 @@ static cs_status attend_scatter(const Geo& g, const CacheView& cv, int32_t layer
   // the scatter of the fresh rows runs inside the attention's first launch
   const ScatterJob job{k_fresh, v_fresh};
   for (int pass = 0; pass < 2; ++pass) {  // sizes of every launch first, then the launches
+    if (pass == 1 && debug_validate()) {
+      cs_status st = check_selection(g, sel_idx, n_sel, s);
+      if (st) return st;
+    }
     cs_status st = launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, false, out, lse,
                                     workspace, s, pass == 0, &job);
     if (st) return st;
@@ -283,6 +331,10 @@ static cs_status attend_scatter_rope(const cs_geometry* gp, const Geo& g, const 
   void* q_ws = (char*)workspace + att;
   for (int pass = 0; pass < 2; ++pass) {  // sizes of every launch first, then the launches
     const bool check = pass == 0;
+    if (!check && debug_validate()) {
+      st = check_selection(g, sel_idx, n_sel, s);
+      if (st) return st;
+    }
     st = launch_rope_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords,
                              theta.data(), q_ws, s, check);
     if (!st)

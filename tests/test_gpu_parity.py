@@ -456,6 +456,51 @@ def test_rebase_extreme_offsets():
     assert np.array_equal(to_host(K2, w.dtype), to_host(K, w.dtype))
 
 
+def test_debug_validation_of_the_selection(monkeypatch):
+    """CS_DEBUG_VALIDATE=1: an unsorted or out-of-range sel_idx is rejected with
+    CS_ERR_INVALID_ARGUMENT before any other work is enqueued (the caches stay
+    untouched), and a valid one gives the result of the unchecked call."""
+    w = ragged(n_layers=2, chunk_lens=(100, 130, 103, 167))
+    log("case debug validation of sel_idx")
+    d = oracle.inputs.build(w)
+    b = B()
+    geo = b.Geo.from_workload(w)
+    rng = np.random.default_rng(4)
+    good = np.sort(rng.choice(np.arange(w.cs1, w.n_tokens), 57, replace=False)).astype(np.int32)
+    k = len(good)
+    unsorted = good.copy()
+    unsorted[[10, 11]] = unsorted[[11, 10]]
+    outside = good.copy()
+    outside[-1] = w.n_tokens
+    ws = torch.empty(b.selective_attend_scatter_workspace(geo, k, w.n_layers), dtype=torch.uint8, device="cuda")
+    Q, KF, VF = to_dev(d["q_fresh"], w.dtype), to_dev(d["k_fresh"], w.dtype), to_dev(d["v_fresh"], w.dtype)
+
+    def call(sel):
+        K, V = to_dev(d["k_stored"], w.dtype), to_dev(d["v_stored"], w.dtype)
+        out = empty((w.n_layers, w.n_q_heads, k, w.head_dim), w.dtype)
+        S = torch.from_numpy(sel).cuda()
+        try:
+            b.selective_attend_scatter(geo, K, V, 0, w.n_layers, S, k, Q, KF, VF, out, None, ws)
+        finally:
+            torch.cuda.synchronize()
+        return K, V, out
+
+    plain = call(good)
+    monkeypatch.setenv("CS_DEBUG_VALIDATE", "1")
+    for sel, msg in ((unsorted, "ascending"), (outside, "outside")):
+        K, V = to_dev(d["k_stored"], w.dtype), to_dev(d["v_stored"], w.dtype)
+        out = empty((w.n_layers, w.n_q_heads, k, w.head_dim), w.dtype)
+        with pytest.raises(b.CsError) as err:
+            b.selective_attend_scatter(geo, K, V, 0, w.n_layers, torch.from_numpy(sel).cuda(), k, Q, KF, VF, out,
+                                       None, ws)
+        torch.cuda.synchronize()
+        assert err.value.code == b.CS_ERR_INVALID_ARGUMENT and msg in str(err.value)
+        assert np.array_equal(to_host(K, w.dtype), d["k_stored"]) and np.array_equal(to_host(V, w.dtype), d["v_stored"])
+    checked = call(good)
+    for x, y in zip(plain, checked):
+        assert np.array_equal(to_host(x, w.dtype), to_host(y, w.dtype))
+
+
 def test_workspace_reuse_and_garbage_workspace():
     """Partial results of cut row tiles live in the caller's workspace: a workspace full of
     garbage must work, and repeated calls on one workspace must give
