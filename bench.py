@@ -139,7 +139,7 @@ def run_compose(inp, w, rho, binding, torch, out, lse, sel, scores, ws, batched,
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the library has no "
               f"multi-GPU path: run with --gpus 1", file=sys.stderr)
         sys.exit(2)
     import torch

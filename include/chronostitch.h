@@ -53,7 +53,7 @@ extern "C" {
 typedef enum {
   CS_OK = 0,
   CS_ERR_INVALID_ARGUMENT = 1,   /* a pointer, size or value is out of its documented range */
-  CS_ERR_UNSUPPORTED = 2,        /* a valid request this build does not implement             */
+  CS_ERR_UNSUPPORTED = 2,        /* a valid request this library does not implement           */
   CS_ERR_WORKSPACE_TOO_SMALL = 3,/* workspace_bytes is below the *_workspace query's answer    */
   CS_ERR_HIP = 4                 /* a HIP runtime call or kernel launch failed                 */
 } cs_status;
