@@ -59,6 +59,8 @@ def parse():
                    help="steps also timed on the cache held as one buffer per chunk (0: skip)")
     p.add_argument("--batched-steps", type=int, default=3,
                    help="steps also timed with one batched attention call over all layers (0: skip)")
+    p.add_argument("--graph-steps", type=int, default=3,
+                   help="steps of the per-layer composition captured once into a HIP graph and replayed (0: skip)")
     p.add_argument("--sweep", choices=("none", "rebase", "attention"), default="none",
                    help="rebase: 8k/65k/262k-token K caches with and without a cache flush, and the "
                         "per-token (scalar re-basing) kernel on the 65k cache; "
@@ -169,9 +171,10 @@ def main():
     paged = None
     if args.paged_steps > 0:
         paged = bench_rho(inp, w, rho, args.paged_steps, 1, binding, torch, False, paged=True)
+    graph = bench_graph(inp, w, rho, args.graph_steps, binding, torch) if args.graph_steps > 0 else None
     gemm = gemm_context(torch) if args.gemm_context else None
     cpu = cpu_baseline(w, rho) if args.cpu_baseline else None
-    emit(args, w, rho, result, rho1, cpu, other, fused, paged, gemm)
+    emit(args, w, rho, result, rho1, cpu, other, fused, paged, gemm, graph)
 
 
 def gemm_context(torch, m=8192, n=8192, k=16384, reps=10):
@@ -265,6 +268,54 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, 
     for name, (cnt, tot) in sorted(trace.items(), key=lambda kv: -kv[1][1]):
         log(f"    {name:24s} launches {cnt:5d}  avg {tot / cnt * 1e3:9.1f} us  total/step {tot / steps:8.3f} ms")
     return res
+
+
+def bench_graph(inp, w, rho, steps, binding, torch):
+    """The per-layer composition captured once into a HIP graph and replayed:
+    the same kernels, launched by the graph instead of the host.  Caches are
+    restored by eager copies before every replay (untimed), and every replay
+    is checked bit-identical to an eager composition."""
+    b = binding
+    n = w.n_candidates
+    scores = torch.empty(n, dtype=torch.float32, device="cuda")
+    sel = torch.empty(n, dtype=torch.int32, device="cuda")
+    k = b.score_deviation_topk(inp.geo, inp.K, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
+    out = torch.empty((w.n_layers, w.n_q_heads, k, w.head_dim), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((w.n_layers, w.n_q_heads, k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(b.selective_attend_scatter_workspace(inp.geo, k, 1), 1), dtype=torch.uint8, device="cuda")
+
+    def restore():
+        inp.K.copy_(inp.K0)
+        inp.V.copy_(inp.V0)
+
+    restore()
+    run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, False)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (inp.K, inp.V, out, lse)]
+    restore()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, False)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    times, identical = [], True
+    for _ in range(steps + 1):   # the first replay is a warm-up
+        restore()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        busy_gpu(torch)
+        e0.record(stream)
+        graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+        identical = identical and all(torch.equal(x, y) for x, y in zip((inp.K, inp.V, out, lse), ref))
+    del graph
+    ms = float(np.median(times[1:]))
+    log(f"[bench] rho={rho}: graph-replayed compose median {ms:.3f} ms, replays identical: {identical}")
+    return dict(ms=ms, identical=identical)
 
 
 def _events(torch, stream, fn, reps, before=None):
@@ -479,7 +530,7 @@ def _traffic(kernel):
         return None
 
 
-def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=None):
+def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=None, graph=None):
     tr = r["trace"]
     steps = r["steps"]
     attn_n, attn_ms = tr.get("sel_attn_mfma", (0, 0.0))
@@ -550,6 +601,9 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=No
         for key, name in (("paged_sel_attn_us", "sel_attn_mfma"), ("paged_rebase_us", "rebase_bf16_d128")):
             if name in pt:
                 line[key] = round(pt[name][1] / pt[name][0] * 1e3, 2)
+    if graph is not None:
+        line["graph_compose_ms"] = round(graph["ms"], 4)
+        line["graph_replays_identical"] = graph["identical"]
     if rho1 is not None:
         line["rho1_compose_ms"] = round(rho1["ms"], 3)
         line["rho1_over_rho_speedup"] = round(rho1["ms"] / r["ms"], 3)

@@ -501,6 +501,56 @@ def test_debug_validation_of_the_selection(monkeypatch):
         assert np.array_equal(to_host(x, w.dtype), to_host(y, w.dtype))
 
 
+def test_graph_capture_replays_the_composition():
+    """The whole composition (re-basing, scoring and selection, one attention
+    call per layer) captured into a HIP graph: the library enqueues only kernel
+    launches, so the graph replays it.  Every replay, with the caches restored
+    by eager copies in between, is bit-identical to the eager composition."""
+    w = ragged(n_layers=3, chunk_lens=(256, 320, 384, 200), G=8, Hkv=2)
+    log("case graph capture of the composition")
+    d = oracle.inputs.build(w)
+    b = B()
+    geo = b.Geo.from_workload(w)
+    K0, V0 = to_dev(d["k_stored"], w.dtype), to_dev(d["v_stored"], w.dtype)
+    Q, KF, VF = to_dev(d["q_fresh"], w.dtype), to_dev(d["k_fresh"], w.dtype), to_dev(d["v_fresh"], w.dtype)
+    K, V = K0.clone(), V0.clone()
+    n, rho = w.n_candidates, 0.3
+    k = oracle.select.n_select(rho, n)
+    scores = torch.empty(n, dtype=torch.float32, device="cuda")
+    sel = torch.empty(n, dtype=torch.int32, device="cuda")
+    out = empty((w.n_layers, w.n_q_heads, k, w.head_dim), w.dtype)
+    lse = torch.empty((w.n_layers, w.n_q_heads, k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(b.selective_attend_scatter_workspace(geo, k, 1), dtype=torch.uint8, device="cuda")
+    off = d["chunk_offsets"]
+
+    def compose():
+        b.compose_rebase_k(geo, K, off)
+        assert b.score_deviation_topk(geo, K, w.score_layer, KF[w.score_layer], rho, scores, sel) == k
+        for layer in range(w.n_layers):
+            b.selective_attend_scatter(geo, K, V, layer, layer + 1, sel, k, Q, KF, VF, out, lse, ws)
+
+    compose()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (K, V, out, lse, sel)]
+    K.copy_(K0)
+    V.copy_(V0)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        compose()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        K.copy_(K0)
+        V.copy_(V0)
+        out.zero_()
+        lse.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for got, want in zip((K, V, out, lse, sel), ref):
+            assert torch.equal(got, want), f"replay {rep}"
+
+
 def test_workspace_reuse_and_garbage_workspace():
     """Partial results of cut row tiles live in the caller's workspace: a workspace full of
     garbage must work, and repeated calls on one workspace must give
