@@ -257,6 +257,36 @@ cs_status selective_attend_scatter(const cs_geometry* g, void* k_cache,
                                    size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * selective_attend_scatter_noalloc -- selective_attend_scatter for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the same scatter and
+ * attention with no workspace argument.  It calls no hipMalloc, hipFree or
+ * other allocating routine (kernel tracing is off for its launches).
+ *
+ * Its plan and partial results live in a 64 MiB array of device memory that
+ * the library holds on every GPU it runs on until the process ends; its
+ * device address is looked up once per GPU, on the first call with that GPU
+ * current.  Every call on a GPU shares that GPU's array: calls that overlap
+ * on one GPU (two streams, two threads) race and give wrong results.  Nothing
+ * needs clearing between calls.
+ *
+ * When the call's plan and partials would exceed the array, the key pieces
+ * of long row tiles are made longer (fewer partials), so the output then
+ * differs from selective_attend_scatter's by rounding only (same tolerance);
+ * within the limit it is bit-identical.  A call whose plan alone exceeds the
+ * array returns CS_ERR_UNSUPPORTED before anything is enqueued (this needs
+ * several million selected rows).
+ *
+ * Arguments, layouts and the other errors are those of
+ * selective_attend_scatter (contiguous cache only).                        */
+cs_status selective_attend_scatter_noalloc(const cs_geometry* g, void* k_cache,
+                                           void* v_cache, int32_t layer_begin,
+                                           int32_t layer_end, const int32_t* sel_idx,
+                                           int64_t n_sel, const void* q_fresh,
+                                           const void* k_fresh, const void* v_fresh,
+                                           void* out, float* lse, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Paged cache (Section 2: every chunk is prefilled and stored on its own, and
  * the stored caches are concatenated after re-basing, the step listed after
  * Eq. 6).  The *_paged calls

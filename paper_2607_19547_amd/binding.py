@@ -59,6 +59,7 @@ def lib():
                                                     vp, sz, vp]
         L.selective_attend_scatter.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp,
                                                vp, sz, vp]
+        L.selective_attend_scatter_noalloc.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp, vp]
         L.compose_rebase_k_paged.argtypes = [G, vp, vp, vp, vp, vp]
         L.compose_rebase_k_tokens_paged.argtypes = [G, vp, vp, vp]
         L.score_deviation_topk_paged.argtypes = [G, vp, i32, vp, ctypes.c_double, vp, vp,
@@ -75,6 +76,7 @@ def lib():
         for name in ("compose_rebase_k", "compose_rebase_k_tokens", "score_deviation_topk_workspace",
                      "score_deviation_topk",
                      "selective_attend_scatter_workspace", "selective_attend_scatter",
+                     "selective_attend_scatter_noalloc",
                      "selective_attend_scatter_rope_workspace", "selective_attend_scatter_rope",
                      "compose_rebase_k_paged", "compose_rebase_k_tokens_paged", "score_deviation_topk_paged",
                      "selective_attend_scatter_paged", "selective_attend_scatter_rope_paged",
@@ -177,6 +179,15 @@ def selective_attend_scatter(geo, k_cache, v_cache, layer_begin, layer_end, sel_
                                           int(layer_end), _ptr(sel_idx), int(n_sel), _ptr(q_fresh),
                                           _ptr(k_fresh), _ptr(v_fresh), _ptr(out), _ptr(lse),
                                           _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def selective_attend_scatter_noalloc(geo, k_cache, v_cache, layer_begin, layer_end, sel_idx, n_sel, q_fresh,
+                                     k_fresh, v_fresh, out, lse=None, stream=None):
+    """selective_attend_scatter with the library's own per-GPU scratch array (no workspace)."""
+    _check(lib().selective_attend_scatter_noalloc(geo.ref, _ptr(k_cache), _ptr(v_cache), int(layer_begin),
+                                                  int(layer_end), _ptr(sel_idx), int(n_sel), _ptr(q_fresh),
+                                                  _ptr(k_fresh), _ptr(v_fresh), _ptr(out), _ptr(lse),
+                                                  _stream(stream)))
 
 
 # ---------------------------------------------------------------- tracing

@@ -54,6 +54,10 @@ std::vector<Pending> g_pending;
 std::vector<std::pair<std::string, Acc>> g_acc;
 std::vector<hipEvent_t> g_pool;
 
+// set while a call that must not allocate enqueues on this thread
+thread_local bool t_trace_suppressed = false;
+bool trace_suppressed() { return t_trace_suppressed; }
+
 hipEvent_t take_event() {
   if (!g_pool.empty()) {
     hipEvent_t e = g_pool.back();
@@ -67,6 +71,7 @@ hipEvent_t take_event() {
 }  // namespace
 
 TraceScope::TraceScope(const char* n, hipStream_t s) : name(n), stream(s), a(nullptr), b(nullptr) {
+  if (trace_suppressed()) return;
   std::lock_guard<std::mutex> lk(g_trace_mu);
   if (!g_trace_on) return;
   a = take_event();
@@ -272,20 +277,27 @@ static cs_status check_selection(const Geo& g, const int32_t* sel, int64_t n_sel
   return CS_OK;
 }
 
-static cs_status attend_scatter(const Geo& g, const CacheView& cv, int32_t layer_begin, int32_t layer_end,
-                                const int32_t* sel_idx, int64_t n_sel, const void* q_fresh, const void* k_fresh,
-                                const void* v_fresh, void* out, float* lse, void* workspace, size_t workspace_bytes,
-                                void* stream) {
+static size_t attn_ws_bytes(const AttnPlan& p, int layers) {
+  return p.mfma ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)layers : 0;
+}
+
+// Argument checks of the attention calls that need no HIP runtime call.
+static cs_status attend_scatter_check(const Geo& g, const CacheView& cv, const int32_t* sel_idx,
+                                      const void* q_fresh, const void* k_fresh, const void* v_fresh, void* out,
+                                      const AttnPlan& p) {
   if (!sel_idx || !q_fresh || !k_fresh || !v_fresh || !out)
     return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
-  AttnPlan p = plan_attention(g, n_sel, layer_end - layer_begin);
-  size_t need = p.mfma ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)(layer_end - layer_begin) : 0;
-  if (need && (!workspace || workspace_bytes < need))
-    return fail(CS_ERR_WORKSPACE_TOO_SMALL,
-                "workspace smaller than selective_attend_scatter_workspace() (" + std::to_string(need) +
-                    " bytes)");
   if (cv.paged && p.mfma && !chunks_tile_aligned(g))
     return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
+  return CS_OK;
+}
+
+// Scatter + attention with a plan whose workspace (attn_ws_bytes) is at
+// `workspace`; every argument has been checked.
+static cs_status attend_scatter_planned(const Geo& g, const CacheView& cv, int32_t layer_begin, int32_t layer_end,
+                                        const int32_t* sel_idx, int64_t n_sel, const void* q_fresh,
+                                        const void* k_fresh, const void* v_fresh, void* out, float* lse,
+                                        const AttnPlan& p, void* workspace, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   // the scatter of the fresh rows runs inside the attention's first launch
   const ScatterJob job{k_fresh, v_fresh};
@@ -300,6 +312,78 @@ static cs_status attend_scatter(const Geo& g, const CacheView& cv, int32_t layer
   }
   return CS_OK;
 }
+
+static cs_status attend_scatter(const Geo& g, const CacheView& cv, int32_t layer_begin, int32_t layer_end,
+                                const int32_t* sel_idx, int64_t n_sel, const void* q_fresh, const void* k_fresh,
+                                const void* v_fresh, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  const AttnPlan p = plan_attention(g, n_sel, layer_end - layer_begin);
+  cs_status st = attend_scatter_check(g, cv, sel_idx, q_fresh, k_fresh, v_fresh, out, p);
+  if (st) return st;
+  const size_t need = attn_ws_bytes(p, layer_end - layer_begin);
+  if (need && (!workspace || workspace_bytes < need))
+    return fail(CS_ERR_WORKSPACE_TOO_SMALL,
+                "workspace smaller than selective_attend_scatter_workspace() (" + std::to_string(need) +
+                    " bytes)");
+  return attend_scatter_planned(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, k_fresh, v_fresh, out, lse,
+                                p, workspace, stream);
+}
+
+// ------------------------------------------------------------------ no-allocation variant
+// selective_attend_scatter_noalloc keeps the attention's plan and partials in
+// this array instead of a caller workspace.  Each GPU the library runs on
+// holds its own copy until the process ends; host code reaches it only through
+// the device address hipGetSymbolAddress returns for the current device (the
+// array's name in host code is not a device address).  The kernels write the
+// plan, including its queue counters, before anything reads it, so no call
+// needs the array cleared; calls that overlap on one GPU race on it.
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+constexpr int kScratchDevices = 256;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kScratchDevices];
+
+static cs_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(CS_ERR_HIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kScratchDevices) return fail(CS_ERR_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(CS_ERR_HIP, std::string("hipGetSymbolAddress of the scratch array failed: ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return CS_OK;
+}
+
+// The library's plan, with its partial slots cut down until plan and
+// partials fit in the scratch array (longer key pieces, or none).
+static cs_status noalloc_plan(const Geo& g, int64_t n_sel, int layers, AttnPlan* out) {
+  AttnPlan p = plan_attention(g, n_sel, layers);
+  if (attn_ws_bytes(p, layers) > kNoAllocScratchBytes && p.part_cap > 0) {
+    const size_t slot = p.ws_bytes_per_layer / (size_t)p.part_cap;
+    const size_t room = p.ws_fixed_bytes < kNoAllocScratchBytes ? kNoAllocScratchBytes - p.ws_fixed_bytes : 0;
+    p = plan_attention(g, n_sel, layers, (int64_t)(room / (slot * (size_t)layers)));
+  }
+  const size_t need = attn_ws_bytes(p, layers);
+  if (need > kNoAllocScratchBytes)
+    return fail(CS_ERR_UNSUPPORTED, "selective_attend_scatter_noalloc: the plan needs " + std::to_string(need) +
+                                        " bytes, more than its " + std::to_string(kNoAllocScratchBytes) +
+                                        "-byte scratch array");
+  *out = p;
+  return CS_OK;
+}
+
+// Kernel tracing creates events; calls that must not allocate turn it off on
+// their thread while they enqueue.
+struct TraceSuppress {
+  bool prev;
+  TraceSuppress() : prev(t_trace_suppressed) { t_trace_suppressed = true; }
+  ~TraceSuppress() { t_trace_suppressed = prev; }
+};
 
 // Workspace of the fused-rotary variant: the attention's, then the rotated
 // queries [layers in call][H_q][n_sel][D].
@@ -462,6 +546,31 @@ cs_status selective_attend_scatter(const cs_geometry* gp, void* k_cache, void* v
   if (!k_cache || !v_cache) return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
   return attend_scatter(g, flat_view(k_cache, v_cache), layer_begin, layer_end, sel_idx, n_sel, q_fresh, k_fresh,
                         v_fresh, out, lse, workspace, workspace_bytes, stream);
+}
+
+cs_status selective_attend_scatter_noalloc(const cs_geometry* gp, void* k_cache, void* v_cache,
+                                           int32_t layer_begin, int32_t layer_end, const int32_t* sel_idx,
+                                           int64_t n_sel, const void* q_fresh, const void* k_fresh,
+                                           const void* v_fresh, void* out, float* lse, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (!st) st = check_layers(g, layer_begin, layer_end, n_sel);
+  if (st) return st;
+  if (n_sel == 0 || layer_end == layer_begin) return CS_OK;
+  if (!k_cache || !v_cache) return fail(CS_ERR_INVALID_ARGUMENT, "a required device pointer is NULL");
+  const CacheView cv = flat_view(k_cache, v_cache);
+  AttnPlan p;
+  st = noalloc_plan(g, n_sel, layer_end - layer_begin, &p);
+  if (!st) st = attend_scatter_check(g, cv, sel_idx, q_fresh, k_fresh, v_fresh, out, p);
+  if (st) return st;
+  void* ws = nullptr;
+  if (p.mfma) {
+    st = scratch_address(&ws);
+    if (st) return st;
+  }
+  TraceSuppress no_trace;
+  return attend_scatter_planned(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_fresh, k_fresh, v_fresh, out, lse,
+                                p, ws, stream);
 }
 
 cs_status selective_attend_scatter_paged(const cs_geometry* gp, void* const* k_chunks, void* const* v_chunks,

@@ -1022,7 +1022,7 @@ __global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a, cons
 // ============================================================== planning & launch
 static int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
-AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call) {
+AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call, int64_t max_part_slots) {
   AttnPlan p{};
   // (buffer loads address one [T][128] bf16 plane, plus three tiles of
   // look-ahead, with 32-bit byte offsets)
@@ -1046,7 +1046,10 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call) {
     p.ws_fixed_bytes = 0;
     return p;
   }
-  p.part_cap = (int)std::min<int64_t>(kPartCap, p.n_tiles * g.Hkv * (max_pieces > 1 ? max_pieces : 0));
+  p.part_cap = (int)std::min<int64_t>(std::min<int64_t>(kPartCap, std::max<int64_t>(max_part_slots, 0)),
+                                      p.n_tiles * g.Hkv * (max_pieces > 1 ? max_pieces : 0));
+  // a cut row tile fills at least 2 H_kv slots: fewer slots allow no cut at all
+  if (p.part_cap < 2 * g.Hkv) p.part_cap = 0;
   // item descriptors (4 ints each) after the plan's arrays, one per queue position
   const int nq = n_queues(g.Hkv);
   const int64_t per_q_bound = (p.n_tiles * g.Hkv + p.part_cap + nq - 1) / nq;

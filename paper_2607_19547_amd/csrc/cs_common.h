@@ -227,7 +227,9 @@ struct AttnPlan {
   size_t ws_fixed_bytes;      // per call: tile plan
   size_t ws_bytes_per_layer;  // per layer in the call: partial segments
 };
-AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call);
+// max_part_slots caps the partial slots per layer below the library's own
+// bound (the plan then makes longer key pieces, or none).
+AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call, int64_t max_part_slots = INT64_MAX);
 // Every chunk starts at a multiple of the 64-key tile (a paged cache on the MFMA path needs it).
 bool chunks_tile_aligned(const Geo& g);
 // The fresh K/V rows the attention launch also scatters into the cache

@@ -213,3 +213,20 @@ def test_launch_sizes_beyond_the_grid_limits_are_rejected(built_lib):
     code, text = _code(b.selective_attend_scatter, huge, FAKE, FAKE, 0, 1, FAKE, big, FAKE, FAKE, FAKE, FAKE,
                        stream=0)
     assert code == b.CS_ERR_UNSUPPORTED and "too large" in text
+
+
+def test_noalloc_attention_argument_errors(built_lib):
+    """The no-workspace attention call rejects what selective_attend_scatter rejects, before any HIP call."""
+    g = _geo()
+    f = b.selective_attend_scatter_noalloc
+    assert _code(f, g, FAKE, FAKE, 1, 3, FAKE, 4, FAKE, FAKE, FAKE, FAKE, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    assert _code(f, g, FAKE, FAKE, 0, 1, FAKE, 33, FAKE, FAKE, FAKE, FAKE, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    assert _code(f, g, None, FAKE, 0, 1, FAKE, 4, FAKE, FAKE, FAKE, FAKE, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    assert _code(f, g, FAKE, FAKE, 0, 1, FAKE, 4, None, FAKE, FAKE, FAKE, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    code, text = _code(f, _geo(sections=(2, 3, 4)), FAKE, FAKE, 0, 1, FAKE, 4, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert code == b.CS_ERR_INVALID_ARGUMENT and "sum" in text
+    f(g, None, None, 0, 1, None, 0, None, None, None, None, stream=0)  # nothing to do: OK, no device work
+    T = (1 << 31) - 128
+    huge = b.Geo(36, 16, 2, 128, (16, 24, 24), "bf16", [0, 64, T])
+    code, text = _code(f, huge, FAKE, FAKE, 0, 1, FAKE, 1 << 27, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert code == b.CS_ERR_UNSUPPORTED and "too large" in text
