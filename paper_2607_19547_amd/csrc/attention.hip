@@ -264,28 +264,31 @@ __device__ __forceinline__ int block_reduce(int v, bool is_max, int* red) {
   return r;
 }
 
-// Inclusive prefix sums of x over the 1024 threads, continuing from *base
-// (shared); returns this thread's inclusive sum and advances *base.
+// Inclusive prefix sums (kMax: running maxima) of x over the 1024 threads,
+// continuing from *base (shared); returns this thread's inclusive value and
+// advances *base.
+template <bool kMax = false>
 __device__ __forceinline__ int block_scan(int x, int* wsum, int* base) {
+  auto op = [](int u, int v) { return kMax ? max(u, v) : u + v; };
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
+    if (lane >= o) x = op(x, y);
   }
   if (lane == 63) wsum[wave] = x;
   __syncthreads();
   int off = *base;
-  for (int w = 0; w < wave; ++w) off += wsum[w];
+  for (int w = 0; w < wave; ++w) off = op(off, wsum[w]);
   __syncthreads();
-  if (threadIdx.x == 1023) *base = off + x;
+  if (threadIdx.x == 1023) *base = op(off, x);
   __syncthreads();
-  return off + x;
+  return op(off, x);
 }
 
-// Builds the work plan of one call (one workgroup of 1024 threads).  Thread t
-// handles row tiles t, t + 1024, ... in every pass, so it reads back only
-// what it wrote itself.
+// Builds the work plan of one call (one workgroup of 1024 threads).  The
+// plan's arrays are written and read back by different threads, always with
+// a barrier between.
 struct PlanArgs {
   const int32_t* sel;
   int64_t n_sel, n_tiles, T;
@@ -306,18 +309,30 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   int* const nu = in_lds ? l_nu : pv.nu;
   int* const nsp = in_lds ? l_nsp : pv.nsp;
   const int tid = threadIdx.x;
-  int sum = 0, mx = 0;
-  for (int64_t i = tid; i < n_tiles; i += 1024) {
-    const int64_t t = n_tiles - 1 - i;
-    const int64_t ml = min((t + 1) * RT, n_sel) - 1;
-    const int64_t g = min((int64_t)sel[ml], T - 1);
-    const int v = g < 0 ? 1 : (int)((g + kKT) / kKT);
-    nu[i] = v;
-    sum += v;
-    mx = max(mx, v);
+  // Key tiles of row tile t: up to its last row's token, taken as a running
+  // maximum over t.  For an ascending selection the maximum changes nothing;
+  // for any other list it keeps n_i non-increasing along the longest-first
+  // order, which the placement of the items below relies on (the cut row
+  // tiles lead, and every queue position is written exactly once).
+  int sum = 0;
+  if (tid == 0) s_base = 0;
+  __syncthreads();
+  for (int64_t b = 0; b < n_tiles; b += 1024) {
+    const int64_t t = b + tid;
+    int v = 1;
+    if (t < n_tiles) {
+      const int64_t ml = min((t + 1) * RT, n_sel) - 1;
+      const int64_t g = min((int64_t)sel[ml], T - 1);
+      v = g < 0 ? 1 : (int)((g + kKT) / kKT);
+    }
+    v = block_scan<true>(v, wsum, &s_base);
+    if (t < n_tiles) {
+      nu[n_tiles - 1 - t] = v;
+      sum += v;
+    }
   }
+  const int nmax = s_base;  // (block_scan ends on a barrier)
   const int W1 = block_reduce(sum, false, red);
-  const int nmax = block_reduce(mx, true, red);
   // piece size: about kItemsPerCU items per CU, raised until the partial
   // slots fit in part_cap (no cut at all always fits)
   const int64_t per = (int64_t)kPlanCUs * kItemsPerCU;
@@ -559,7 +574,10 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
   const int lrel = item / per_q;
   const int r = item - lrel * per_q;
   const int4 dsc = *(const int4*)(a.plan + a.desc_off + 4 * r);  // the item's descriptor
-  const int oi = dsc.x, kvl = dsc.y & 0xffff, piece = dsc.y >> 16;
+  const int oi = dsc.x, kvl = dsc.y & 0xffff;
+  // (the plan writes every descriptor in range; this bound only keeps a
+  // damaged plan from addressing outside the plan and the output)
+  if (oi < 0 || oi >= a.n_tiles || kvl * nq + jq >= a.Hkv || dsc.z < 0 || dsc.w < dsc.z) return;
   const int64_t seg_b = dsc.z, seg_e = dsc.w;
   const int kv = kvl * nq + jq;
   const int64_t tile = a.n_tiles - 1 - oi;
@@ -607,10 +625,11 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
 
   const int nsp = pv.nsp[oi];  // for the epilogue
   const bool full = nsp == 1;
+  const int piece = min(dsc.y >> 16, nsp - 1);  // (a bound as above, for a damaged plan only)
   const int64_t m0 = tile * RT;
-  const int64_t m_last = min(m0 + RT, a.n_sel) - 1;
-  const int g_last = min((int64_t)a.sel[m_last], a.T - 1);
-  const int key_end = min((int)(seg_e * kKT), g_last + 1);
+  // The piece's key tiles end where the plan says: the plan counted them up
+  // to the row tile's last token, so the last tile holds that token.
+  const int key_end = (int)min(seg_e * kKT, a.T);
   const int n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
 
   const int64_t m = m0 + wave * RW + q / G;
@@ -621,10 +640,16 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     if (t >= a.cs1 && t < a.T) g_q = t;
   }
   const bool valid = g_q >= 0;
-  const int64_t mw0 = m0 + wave * RW;
-  const int64_t mw1 = min(mw0 + RW, a.n_sel) - 1;
-  const int g_wmin = mw0 < a.n_sel ? a.sel[mw0] : 0x7fffffff;
-  const int g_wmax = mw0 < a.n_sel ? a.sel[mw1] : -1;
+  // the wavefront's smallest and largest token: masking starts at the tile
+  // that reaches past the smallest, arithmetic stops after the largest
+  int g_wmin = valid ? g_q : 0x7fffffff, g_wmax = g_q;
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) {
+    g_wmin = min(g_wmin, __shfl_xor(g_wmin, o));
+    g_wmax = max(g_wmax, __shfl_xor(g_wmax, o));
+  }
+  g_wmin = __builtin_amdgcn_readfirstlane(g_wmin);
+  g_wmax = __builtin_amdgcn_readfirstlane(g_wmax);
 
   bf16x8 qb[8];
   if (valid) {
