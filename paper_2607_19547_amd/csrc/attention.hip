@@ -20,12 +20,13 @@
 //
 // Work is scheduled on the device: a planning workgroup (in the same launch
 // as the scatter of the fresh rows) lists the (row tile, KV head, key piece)
-// items, longest row tiles first, with a descriptor per item, and each
-// attention workgroup runs one item: the first three quarters of every queue
-// are dealt by workgroup position, the rest through an atomic counter per
-// queue.  Row tiles too long for an even schedule are cut into key pieces
-// whose partial (O, max, sum) a combine kernel merges in a fixed order, so
-// results do not depend on timing.
+// items, longest row tiles first, with a descriptor per item.  The attention
+// launch is one resident workgroup per CU; each takes items from its queue
+// through an atomic counter until every queue is empty, fetching the next
+// item's first key tiles while the current item's results are written.  Row
+// tiles too long for an even schedule are cut into key pieces whose partial
+// (O, max, sum) a combine kernel merges in a fixed order, so results do not
+// depend on timing.
 //
 // Generic path: one wavefront per (row, query head), float32 arithmetic, any
 // head_dim <= 512 and either storage dtype.
@@ -197,21 +198,18 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_bu
 // Work decomposition.  Row tiles are ordered longest first (they end at the
 // highest selected tokens); row tile i needs n_i = ceil((g_last + 1) / 64)
 // key tiles.  A row tile longer than the piece size S is cut into
-// ceil(n_i / S) near-equal pieces over its keys.  An item is one piece of one
-// row tile for one KV head.  Items sit in nq queues, queue j holding the KV
-// heads kv = j (mod nq), and the launch places queue j on the XCDs x = j
-// (mod nq), so an XCD's L2 serves few KV heads.  The first 3/4 of every
-// queue is dealt to those XCDs in turn by workgroup position; the rest is
-// handed out through an atomic counter per queue to the workgroups that
-// follow on every XCD (an XCD whose queue is empty takes from the others, and
-// surplus workgroups exit), so XCDs that run faster take more of the tail.
-// Within a queue, the pieces of cut row tiles come first,
-// piece-major (piece 0 of every cut row tile, then piece 1, ...: workgroups
-// running side by side read the same keys), then the uncut row tiles, longest
-// first; the counter-dealt last quarter is then reordered longest first, so a
-// launch ends on its shortest items.  The pieces of a cut row tile leave
-// partial (O, max, sum) in fixed workspace slots that sel_attn_combine merges
-// in piece order.
+// ceil(n_i / S) pieces at key tiles 0, S, 2S, ..., so piece j of every cut
+// row tile covers the same keys.  An item is one piece of one row tile for
+// one KV head.  Items sit in nq queues, queue j holding the KV heads
+// kv = j (mod nq), and the workgroups of XCDs x = j (mod nq) take from queue
+// j, so an XCD's L2 serves few KV heads; a workgroup whose queue is empty
+// takes from the others, so XCDs that run faster take more.  Within a queue,
+// the pieces of cut row tiles come first, piece-major (piece 0 of every cut
+// row tile, then piece 1, ...: workgroups running side by side read the same
+// keys, which the L2 then serves once), then the uncut row tiles, longest
+// first; the last quarter is then reordered longest first, so a launch ends
+// on its shortest items.  The pieces of a cut row tile leave partial (O, max,
+// sum) in fixed workspace slots that sel_attn_combine merges in piece order.
 constexpr int kPlanHdr = 16;    // header ints, see PlanView
 constexpr int kPlanCUs = 256;   // CU count S is derived from (a constant: results do not depend on the device)
 constexpr int kItemsPerCU = 6;  // target items per CU when row tiles must be cut
@@ -224,7 +222,7 @@ constexpr int kXcds = 8;
 
 struct PlanView {
   int* hdr;   // [0, 8) queue counters, [8] nq, [9] S, [10] cut row tiles, [11] most pieces,
-              // [12] items per queue and layer, [13] workgroup rounds placed by position,
+              // [12] items per queue and layer,
               // [14] offset of the item descriptors (ints from the plan's start)
   int* nu;    // [n_tiles] key tiles of row tile i (longest first)
   int* nsp;   // [n_tiles] pieces of row tile i
@@ -398,12 +396,9 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   }
   if (tid == 0) {
     const int per_q = s_base + (int)(n_tiles - n_cut) * kvq;
-    const int share = kXcds / nq;
-    const int rounds = (int)((int64_t)per_q * layers * 3 / 4 / share);  // placed by position
     pv.ppre[0] = 0;
     pv.pj[0] = l_pj[0] = 0;
-    for (int k = 0; k < kXcds; ++k) pv.hdr[k] = rounds * share;  // first item of the dynamic tail
-    pv.hdr[13] = rounds;
+    for (int k = 0; k < kXcds; ++k) pv.hdr[k] = 0;  // the queues' claim counters
     pv.hdr[8] = nq;
     pv.hdr[9] = S;
     pv.hdr[10] = n_cut;
@@ -438,7 +433,7 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
     if (np > 1) {
       for (int j = 0; j < np; ++j) {
         const int cnt = (l_pj[j + 1] - l_pj[j]) / kvq;
-        const int b = (int)((int64_t)j * v / np), e = (int)((int64_t)(j + 1) * v / np);
+        const int b = j * S, e = min((j + 1) * S, v);  // the same key range for piece j of every row tile
         for (int kvl = 0; kvl < kvq; ++kvl) put(l_pj[j] + kvl * cnt + (int)i, make_int4((int)i, kvl | (j << 16), b, e));
       }
     } else {
@@ -519,43 +514,140 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     else if constexpr (decltype(B)::value == 2) return lo_v2;
     else return lo_v3;
   };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
 
-  __shared__ int s_take[2];
-  const PlanView pv = plan_view(a.plan, a.n_tiles);
-  const int nq = pv.hdr[8], n_cut = pv.hdr[10], nj = pv.hdr[11], per_q = pv.hdr[12], rounds = pv.hdr[13];
-  const int total_q = per_q * a.layers;
-  // Workgroup b runs on XCD b mod 8; the XCDs x = j (mod nq) share queue j.
-  const int xs = blockIdx.x % kXcds, share = kXcds / nq;
-  const int kround = blockIdx.x / kXcds;
-  int jq = xs % nq, item;
-  if (kround < rounds) {  // placed: the queue's items in turn
-    item = kround * share + xs / nq;
-  } else {  // the tail: the next item of this XCD's queue, else of another
-    if (threadIdx.x == 0) {
-      int got = -1, j = jq;
-      for (int t = 0; t < nq; ++t) {
-        const int v = atomicAdd(&pv.hdr[j], 1);
-        if (v < total_q) {
-          got = v;
-          break;
-        }
+  // The workgroup stays resident and takes items one after another from its
+  // XCD's queue (then from the others'), through one atomic counter per
+  // queue.  The next item is claimed while an item's results are written, and
+  // its first two key tiles are fetched before its queries are loaded.
+  //
+  // Registers are the limit of this kernel (two wavefronts per SIMD), so
+  // nothing that only the per-item code needs is kept in registers across the
+  // tile loop: the item's fields sit in LDS, the kernel arguments are read
+  // again from the argument segment, and lane-derived addresses are formed
+  // from a lane index read afresh (an opaque value the compiler cannot hoist
+  // out of the item loop).
+  __shared__ int s_claim[2];
+  __shared__ int s_it[8];  // the current item: layer in call, row tile, KV head, piece, first and end key
+  typedef const __attribute__((address_space(4))) AttnArgs* ArgPtr;  // the argument segment (scalar loads)
+  const ArgPtr argp = (ArgPtr)__builtin_amdgcn_kernarg_segment_ptr();
+  auto args = [&]() -> AttnArgs {  // the arguments, read anew where they are used
+    ArgPtr p = argp;
+    asm volatile("" : "+s"(p));
+    return *(const AttnArgs*)p;
+  };
+  auto it_field = [&](int k) { return __builtin_amdgcn_readfirstlane(s_it[k]); };  // (uniform)
+  auto lane_id = []() {
+    int l;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+    return l;
+  };
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int jq;  // this workgroup's queue: workgroup b runs on XCD b mod 8, and the XCDs x = j (mod nq) share queue j
+  {
+    const PlanView pv = plan_view(a.plan, a.n_tiles);
+    jq = (blockIdx.x % kXcds) % pv.hdr[8];
+  }
+  // A claim: the queue position got from this workgroup's queue, or, past
+  // its end, the next queue's first free position (whole workgroup; thread 0
+  // claims).  -1 when every queue is empty.
+  auto claim_rest = [&](const AttnArgs& A, int got) -> int {
+    const PlanView pv = plan_view(A.plan, A.n_tiles);
+    const int nq = pv.hdr[8], total_q = pv.hdr[12] * A.layers;
+    if (tid == 0) {
+      int j = jq;
+      for (int t = 1; got >= total_q && t < nq; ++t) {
         j = j + 1 == nq ? 0 : j + 1;
+        got = atomicAdd(&pv.hdr[j], 1);
       }
-      s_take[0] = got;
-      s_take[1] = j;
+      s_claim[0] = got < total_q ? got : -1;
+      s_claim[1] = j;
     }
     __syncthreads();
-    item = __builtin_amdgcn_readfirstlane(s_take[0]);
-    jq = __builtin_amdgcn_readfirstlane(s_take[1]);
-    if (item < 0) return;  // whole workgroup: every queue is empty
-  }
-  if (item >= total_q) return;  // (placed rounds never reach past the queue)
+    const int it = __builtin_amdgcn_readfirstlane(s_claim[0]);
+    jq = __builtin_amdgcn_readfirstlane(s_claim[1]);
+    __syncthreads();  // s_claim is reused by the next claim
+    return it;
+  };
+  auto claim_one = [&](const AttnArgs& A) -> int {
+    int got = 0;
+    if (tid == 0) got = atomicAdd(&plan_view(A.plan, A.n_tiles).hdr[jq], 1);
+    return claim_rest(A, got);
+  };
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int q = lane & 31, hi = lane >> 5;
-  const StageOffsets so = stage_offsets(wave, lane);
+  // Key tiles are fetched in ascending order.  A contiguous cache is one
+  // buffer range per plane; in a paged cache every 64-key tile lies inside one
+  // chunk (chunk starts are multiples of 64), and the range follows the chunk
+  // of the tile being fetched.  Rows past a range read as zeros.
+  const StageOffsets so = stage_offsets(wave, tid & 63);
+  __amdgpu_buffer_rsrc_t rk, rv;
+  int dma_c = 0, dma_first = 0, dma_next = 0x7fffffff;
+  int64_t dma_plane = 0;
+  auto use_chunk = [&](int c) {
+    if constexpr (kPaged) {
+      const int s0 = rows.start[c], len = rows.start[c + 1] - s0;
+      rk = plane_rsrc(rows.k[c] + dma_plane * len * kRow, len);
+      rv = plane_rsrc(rows.v[c] + dma_plane * len * kRow, len);
+      dma_c = c;
+      dma_first = s0;
+      dma_next = c + 1 < rows.n ? rows.start[c + 1] : 0x7fffffff;
+    }
+  };
+  auto fetch = [&](int kt, char* Kd, char* Vd) {
+    if constexpr (kPaged) {
+      if (kt >= dma_next) {
+        int c = dma_c + 1;
+        while (c + 1 < rows.n && rows.start[c + 1] <= kt) ++c;
+        use_chunk(c);
+      }
+    }
+    stage_dma(rk, rv, so, kt - dma_first, Kd, Vd, wave);
+  };
+  // An item's fields from its descriptor {row tile (longest-first order), KV
+  // head in the queue | piece << 16, key tiles [b, e)} into s_it (thread 0),
+  // then the buffer ranges of its plane and its key tiles 0 and 1 into ring
+  // slots 0 and 1.  False for a damaged plan entry (never for a plan the
+  // planning kernel wrote).
+  auto start_item = [&](const AttnArgs& A, int item) -> bool {
+    const PlanView pv = plan_view(A.plan, A.n_tiles);
+    const int per_q = pv.hdr[12], nq = pv.hdr[8];
+    const int lrel = item / per_q;
+    const int4 dsc = *(const int4*)(A.plan + A.desc_off + 4 * (item - lrel * per_q));
+    const int oi = dsc.x, kv = (dsc.y & 0xffff) * nq + jq;
+    if (oi < 0 || oi >= A.n_tiles || kv >= A.Hkv || dsc.z < 0 || dsc.w < dsc.z) return false;
+    const int key_begin = (int)min((int64_t)dsc.z * kKT, A.T);
+    if (tid == 0) {
+      s_it[0] = lrel;
+      s_it[1] = oi;
+      s_it[2] = kv;
+      s_it[3] = dsc.y >> 16;
+      s_it[4] = key_begin;
+      s_it[5] = (int)min((int64_t)dsc.w * kKT, A.T);  // the last tile holds the row tile's last token
+    }
+    dma_plane = (int64_t)(A.lb + lrel) * A.Hkv + kv;
+    if constexpr (kPaged) {
+      use_chunk(__builtin_amdgcn_readfirstlane(rows.chunk_of(key_begin)));
+    } else {
+      rk = plane_rsrc(rows.k + dma_plane * A.T * kRow, A.T);
+      rv = plane_rsrc(rows.v + dma_plane * A.T * kRow, A.T);
+    }
+    fetch(key_begin, up_k0, lo_v0);
+    fetch(key_begin + kKT, up_k1, lo_v1);
+    return true;
+  };
+  auto next_item = [&](const AttnArgs& A, int got) {  // claims until an item starts; false when none is left
+    int item = claim_rest(A, got);
+    while (item >= 0 && !start_item(A, item)) item = claim_one(A);
+    __syncthreads();  // s_it is written
+    return item >= 0;
+  };
+
   // per-lane LDS offsets of the MFMA operands
   int koff[8];  // K: row q, chunk 2s + hi  (row 32 + q has the same swizzle), plus kHiLds
+  const int lane = tid & 63, q = lane & 31, hi = lane >> 5;
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
     koff[s] = q * kRow + 16 * ((2 * s + hi) ^ (q & 15));
@@ -571,319 +663,292 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
   const float sc = a.scale_log2;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  const int lrel = item / per_q;
-  const int r = item - lrel * per_q;
-  const int4 dsc = *(const int4*)(a.plan + a.desc_off + 4 * r);  // the item's descriptor
-  const int oi = dsc.x, kvl = dsc.y & 0xffff;
-  // (the plan writes every descriptor in range; this bound only keeps a
-  // damaged plan from addressing outside the plan and the output)
-  if (oi < 0 || oi >= a.n_tiles || kvl * nq + jq >= a.Hkv || dsc.z < 0 || dsc.w < dsc.z) return;
-  const int64_t seg_b = dsc.z, seg_e = dsc.w;
-  const int kv = kvl * nq + jq;
-  const int64_t tile = a.n_tiles - 1 - oi;
-  const int layer = a.lb + lrel;
-  const int key_begin = (int)(seg_b * kKT);
+  if (!next_item(a, tid == 0 ? atomicAdd(&plan_view(a.plan, a.n_tiles).hdr[jq], 1) : 0)) return;  // every queue is empty
 
-  // Key tiles are fetched in ascending order, the first three as soon as the
-  // descriptor is known (the item's remaining loads overlap them).  A
-  // contiguous cache is one buffer range per plane; in a paged cache every
-  // 64-key tile lies inside one chunk (chunk starts are multiples of 64), and
-  // the range follows the chunk of the tile being fetched.  Rows past a range
-  // read as zeros.
-  const int64_t plane = (int64_t)layer * a.Hkv + kv;
-  __amdgpu_buffer_rsrc_t rk, rv;
-  int dma_c = 0, dma_first = 0, dma_next = 0x7fffffff;
-  auto use_chunk = [&](int c) {
-    if constexpr (kPaged) {
-      const int s0 = rows.start[c], len = rows.start[c + 1] - s0;
-      rk = plane_rsrc(rows.k[c] + plane * len * kRow, len);
-      rv = plane_rsrc(rows.v[c] + plane * len * kRow, len);
-      dma_c = c;
-      dma_first = s0;
-      dma_next = c + 1 < rows.n ? rows.start[c + 1] : 0x7fffffff;
-    }
-  };
-  if constexpr (kPaged) {
-    use_chunk(__builtin_amdgcn_readfirstlane(rows.chunk_of(key_begin)));
-  } else {
-    rk = plane_rsrc(rows.k + plane * a.T * kRow, a.T);
-    rv = plane_rsrc(rows.v + plane * a.T * kRow, a.T);
-  }
-  auto fetch = [&](int kt, char* Kd, char* Vd) {
-    if constexpr (kPaged) {
-      if (kt >= dma_next) {
-        int c = dma_c + 1;
-        while (c + 1 < rows.n && rows.start[c + 1] <= kt) ++c;
-        use_chunk(c);
+  while (true) {
+    int g_q = -1, g_wmin, g_wmax, key_begin, n_kt;
+    bf16x8 qb[8];
+    {
+      const AttnArgs A = args();
+      key_begin = it_field(4);
+      fetch(key_begin + 2 * kKT, up_k2, lo_v2);
+      const int lrel = it_field(0), oi = it_field(1), kv = it_field(2);
+      const int key_end = it_field(5);
+      n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
+      const int ln = lane_id(), lq = ln & 31;
+      const int64_t m = (A.n_tiles - 1 - oi) * RT + wave * RW + lq / G;
+      const int h = kv * G + lq % G;
+      if (m < A.n_sel) {
+        const int t = A.sel[m];
+        if (t >= A.cs1 && t < A.T) g_q = t;
+      }
+      // the wavefront's smallest and largest token: masking starts at the
+      // tile that reaches past the smallest, arithmetic stops after the largest
+      g_wmin = g_q >= 0 ? g_q : 0x7fffffff;
+      g_wmax = g_q;
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) {
+        g_wmin = min(g_wmin, __shfl_xor(g_wmin, o));
+        g_wmax = max(g_wmax, __shfl_xor(g_wmax, o));
+      }
+      g_wmin = __builtin_amdgcn_readfirstlane(g_wmin);
+      g_wmax = __builtin_amdgcn_readfirstlane(g_wmax);
+      if (g_q >= 0) {
+        const int64_t qrow = A.q_by_slot ? ((int64_t)lrel * A.Hq + h) * A.n_sel + m
+                                         : ((int64_t)(A.lb + lrel) * A.Hq + h) * A.n + (g_q - A.cs1);
+        const uint16_t* qp = A.q + qrow * 128 + 8 * (ln >> 5);
+#pragma unroll
+        for (int s = 0; s < 8; ++s) qb[s] = *(const bf16x8*)(qp + 16 * s);
+      } else {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) qb[s] = bf16x8{};
       }
     }
-    stage_dma(rk, rv, so, kt - dma_first, Kd, Vd, wave);
-  };
-  fetch(key_begin, up_k0, lo_v0);
-  fetch(key_begin + kKT, up_k1, lo_v1);
-  fetch(key_begin + 2 * kKT, up_k2, lo_v2);
 
-  const int nsp = pv.nsp[oi];  // for the epilogue
-  const bool full = nsp == 1;
-  const int piece = min(dsc.y >> 16, nsp - 1);  // (a bound as above, for a damaged plan only)
-  const int64_t m0 = tile * RT;
-  // The piece's key tiles end where the plan says: the plan counted them up
-  // to the row tile's last token, so the last tile holds that token.
-  const int key_end = (int)min(seg_e * kKT, a.T);
-  const int n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
+    f32x16 o[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) o[d] = f32x16{};
+    float m_use = -INFINITY, l_run = 0.f;
 
-  const int64_t m = m0 + wave * RW + q / G;
-  const int h = kv * G + q % G;
-  int g_q = -1;
-  if (m < a.n_sel) {
-    const int t = a.sel[m];
-    if (t >= a.cs1 && t < a.T) g_q = t;
-  }
-  const bool valid = g_q >= 0;
-  // the wavefront's smallest and largest token: masking starts at the tile
-  // that reaches past the smallest, arithmetic stops after the largest
-  int g_wmin = valid ? g_q : 0x7fffffff, g_wmax = g_q;
+    // S^T = K Q^T for the tile in LDS buffer B
+    auto qk = [&](auto B, f32x16& s0, f32x16& s1) {
+      const char* K = kbuf(B);
+      s0 = f32x16{};
+      s1 = f32x16{};
 #pragma unroll
-  for (int o = 1; o < 32; o <<= 1) {
-    g_wmin = min(g_wmin, __shfl_xor(g_wmin, o));
-    g_wmax = max(g_wmax, __shfl_xor(g_wmax, o));
-  }
-  g_wmin = __builtin_amdgcn_readfirstlane(g_wmin);
-  g_wmax = __builtin_amdgcn_readfirstlane(g_wmax);
-
-  bf16x8 qb[8];
-  if (valid) {
-    const int64_t qrow = a.q_by_slot ? ((int64_t)lrel * a.Hq + h) * a.n_sel + m
-                                     : ((int64_t)layer * a.Hq + h) * a.n + (g_q - a.cs1);
-    const uint16_t* qp = a.q + qrow * 128 + 8 * hi;
-#pragma unroll
-    for (int s = 0; s < 8; ++s) qb[s] = *(const bf16x8*)(qp + 16 * s);
-  } else {
-#pragma unroll
-    for (int s = 0; s < 8; ++s) qb[s] = bf16x8{};
-  }
-
-  f32x16 o[4];
-#pragma unroll
-  for (int d = 0; d < 4; ++d) o[d] = f32x16{};
-  float m_use = -INFINITY, l_run = 0.f;
-
-  // S^T = K Q^T for the tile in LDS buffer B
-  auto qk = [&](auto B, f32x16& s0, f32x16& s1) {
-    const char* K = kbuf(B);
-    s0 = f32x16{};
-    s1 = f32x16{};
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
-      const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], s1, 0, 0, 0);
-    }
-  };
-
-  // Causal mask and running max of the tile starting at key kt; rescales the
-  // accumulators when the max grew by more than 2^8.
-  auto mask_max = [&](int kt, f32x16& s0, f32x16& s1) {
-    // accumulator register r of block b holds key kt + 32b + 8(r/4) + 4hi + r%4
-    if (kt + kKT - 1 > g_wmin) {
-      const int lim = g_q - kt - 4 * hi;
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const int off = 8 * (rr >> 2) + (rr & 3);
-        if (off > lim) s0[rr] = -INFINITY;
-        if (off + 32 > lim) s1[rr] = -INFINITY;
+      for (int s = 0; s < 8; ++s) {
+        const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
+        const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], s1, 0, 0, 0);
       }
-    }
-    // max tree of three-input maxima (16 instructions), eight independent chains first
-    float t8[8];
-#pragma unroll
-    for (int rr = 0; rr < 8; ++rr) t8[rr] = fmaxf(fmaxf(s0[rr], s0[rr + 8]), s1[rr]);
-    float t4[4];
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) t4[rr] = fmaxf(fmaxf(t8[2 * rr], t8[2 * rr + 1]), s1[rr + 8]);
-    const float t2a = fmaxf(fmaxf(t4[0], t4[1]), s1[12]), t2b = fmaxf(fmaxf(t4[2], t4[3]), s1[13]);
-    const float mx = fmaxf(fmaxf(fmaxf(t2a, t2b), s1[14]), s1[15]);
-    const float mt = pair_max(mx) * sc;
-    const bool need = mt > m_use + kRescaleLog2;
-    if (__ballot(need)) {
-      const float m_new = need ? mt : m_use;
-      const float alpha = need ? __builtin_amdgcn_exp2f(m_use - m_new) : 1.f;
-      l_run *= alpha;
-#pragma unroll
-      for (int d = 0; d < 4; ++d) o[d] *= alpha;
-      m_use = m_new;
-    }
-  };
+    };
 
-  // Probabilities of the current tile (buffer C), O^T += V^T P^T, and, in
-  // the same straight-line block, k-steps 2..7 of S^T of the next tile
-  // (buffer N; k-steps 0..1 were issued before the running max), so the
-  // exponentials overlap the matrix instructions.
-  auto qk_head = [&](auto N, f32x16& n0, f32x16& n1) {
-    const char* K = kbuf(N);
-    n0 = f32x16{};
-    n1 = f32x16{};
+    // Causal mask and running max of the tile starting at key kt; rescales the
+    // accumulators when the max grew by more than 2^8.
+    auto mask_max = [&](int kt, f32x16& s0, f32x16& s1) {
+      // accumulator register r of block b holds key kt + 32b + 8(r/4) + 4hi + r%4
+      if (kt + kKT - 1 > g_wmin) {
+        const int lim = g_q - kt - 4 * hi;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
-      const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
-      n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
-      n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
-    }
-  };
-  auto exp_pv_qk = [&](auto C, auto N, f32x16& s0, f32x16& s1, f32x16& n0, f32x16& n1) {
-    const char* V = vbuf(C);
-    const char* K = kbuf(N);
-    // LLVM's MFMA / exponential interleave strategy for this block: measured
-    // 1.4% fewer cycles per launch than the default schedule
-    __builtin_amdgcn_iglp_opt(3);
-    const float nm = m_use == -INFINITY ? 0.f : -m_use;
-    bf16x8 pb[4];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const f32x16& sv = ks < 2 ? s0 : s1;
-      const int base = 8 * (ks & 1);
-#pragma unroll
-      for (int x = 0; x < 8; ++x) pb[ks][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sv[base + x], sc, nm));
-      if (ks < 3) {  // k-steps 2(ks+1), 2(ks+1)+1 of the next tile's S^T
-#pragma unroll
-        for (int s = 2 * ks + 2; s < 2 * ks + 4; ++s) {
-          const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
-          const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
-          n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
-          n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
+        for (int rr = 0; rr < 16; ++rr) {
+          const int off = 8 * (rr >> 2) + (rr & 3);
+          if (off > lim) s0[rr] = -INFINITY;
+          if (off + 32 > lim) s1[rr] = -INFINITY;
         }
       }
+      // max tree of three-input maxima (16 instructions), eight independent chains first
+      float t8[8];
 #pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        const char* vp = V + ks * 16 * kRow + voff[d];
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vp));
-        const bf16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vp + 8 * kRow));
-        const bf16x8 va = __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7);
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks], o[d], 0, 0, 0);
+      for (int rr = 0; rr < 8; ++rr) t8[rr] = fmaxf(fmaxf(s0[rr], s0[rr + 8]), s1[rr]);
+      float t4[4];
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) t4[rr] = fmaxf(fmaxf(t8[2 * rr], t8[2 * rr + 1]), s1[rr + 8]);
+      const float t2a = fmaxf(fmaxf(t4[0], t4[1]), s1[12]), t2b = fmaxf(fmaxf(t4[2], t4[3]), s1[13]);
+      const float mx = fmaxf(fmaxf(fmaxf(t2a, t2b), s1[14]), s1[15]);
+      const float mt = pair_max(mx) * sc;
+      const bool need = mt > m_use + kRescaleLog2;
+      if (__ballot(need)) {
+        const float m_new = need ? mt : m_use;
+        const float alpha = need ? __builtin_amdgcn_exp2f(m_use - m_new) : 1.f;
+        l_run *= alpha;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) o[d] *= alpha;
+        m_use = m_new;
       }
-    }
-    // row sum of the bf16 probabilities the PV product used
-    float lsum = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const bf16x2 pp = {pb[ks][2 * x], pb[ks][2 * x + 1]};
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lsum, false);
-      }
-    l_run += lsum;
-  };
+    };
 
-  // One pipeline step: tile i sits in ring slot C, tile i+1 in slot N, and
-  // tile i+3 is fetched by DMA into slot S (read last in step i-1).  Each
-  // wavefront then waits only for the DMA of tile i+2 (its four newest
-  // buffer loads, tile i+3's, may stay in flight) before the barrier.  Past
-  // the end of the key range the fetched rows are never used and the
-  // next-tile product is discarded, which keeps the step free of branches.
-  // A wavefront whose rows all end before tile i skips the arithmetic.
-  auto step = [&](auto C, auto N, auto S, int i, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
-    const int kt = key_begin + i * kKT;
-    fetch(kt + 3 * kKT, kbuf(S), vbuf(S));
-    if (kt <= g_wmax) {
-      qk_head(N, n0, n1);
-      mask_max(kt, c0, c1);
-      exp_pv_qk(C, N, c0, c1, n0, n1);
-    }
-    asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    // Probabilities of the current tile (buffer C), O^T += V^T P^T, and, in
+    // the same straight-line block, k-steps 2..7 of S^T of the next tile
+    // (buffer N; k-steps 0..1 were issued before the running max), so the
+    // exponentials overlap the matrix instructions.
+    auto qk_head = [&](auto N, f32x16& n0, f32x16& n1) {
+      const char* K = kbuf(N);
+      n0 = f32x16{};
+      n1 = f32x16{};
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
+        const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
+        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
+        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
+      }
+      // operand reads two ahead of the products that use them
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    };
+    auto exp_pv_qk = [&](auto C, auto N, f32x16& s0, f32x16& s1, f32x16& n0, f32x16& n1) {
+      const char* V = vbuf(C);
+      const char* K = kbuf(N);
+      // LLVM's MFMA / exponential interleave strategy for this block: measured
+      // 1.4% fewer cycles per launch than the default schedule
+      __builtin_amdgcn_iglp_opt(3);
+      const float nm = m_use == -INFINITY ? 0.f : -m_use;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const f32x16& sv = ks < 2 ? s0 : s1;
+        const int base = 8 * (ks & 1);
+#pragma unroll
+        for (int x = 0; x < 8; ++x) pb[ks][x] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sv[base + x], sc, nm));
+        if (ks < 3) {  // k-steps 2(ks+1), 2(ks+1)+1 of the next tile's S^T
+#pragma unroll
+          for (int s = 2 * ks + 2; s < 2 * ks + 4; ++s) {
+            const bf16x8 k0 = *(const bf16x8*)(K - kHiLds + koff[s]);
+            const bf16x8 k1 = *(const bf16x8*)(K - kHiLds + 32 * kRow + koff[s]);
+            n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qb[s], n0, 0, 0, 0);
+            n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qb[s], n1, 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const char* vp = V + ks * 16 * kRow + voff[d];
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vp));
+          const bf16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vp + 8 * kRow));
+          const bf16x8 va = __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7);
+          o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks], o[d], 0, 0, 0);
+        }
+      }
+      // row sum of the bf16 probabilities the PV product used
+      float lsum = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const bf16x2 pp = {pb[ks][2 * x], pb[ks][2 * x + 1]};
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lsum, false);
+        }
+      l_run += lsum;
+    };
+
+    // One pipeline step: tile i sits in ring slot C, tile i+1 in slot N, and
+    // tile i+3 is fetched by DMA into slot S (read last in step i-1).  Each
+    // wavefront then waits only for the DMA of tile i+2 (its four newest
+    // buffer loads, tile i+3's, may stay in flight) before the barrier.  Past
+    // the end of the key range the fetched rows are never used and the
+    // next-tile product is discarded, which keeps the step free of branches.
+    // A wavefront whose rows all end before tile i skips the arithmetic.
+    auto step = [&](auto C, auto N, auto S, int i, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1) {
+      const int kt = key_begin + i * kKT;
+      fetch(kt + 3 * kKT, kbuf(S), vbuf(S));
+      if (kt <= g_wmax) {
+        qk_head(N, n0, n1);
+        mask_max(kt, c0, c1);
+        exp_pv_qk(C, N, c0, c1, n0, n1);
+      }
+      asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+    };
+
+    f32x16 sa0, sa1, sb0, sb1;
+    asm volatile("s_waitcnt vmcnt(4)" ::: "memory");  // tiles 0 and 1 and the queries have landed
     __builtin_amdgcn_s_barrier();
-  };
+    qk(I0{}, sa0, sa1);
+    for (int i = 0; i < n_kt; i += 4) {
+      step(I0{}, I1{}, I3{}, i, sa0, sa1, sb0, sb1);
+      if (i + 1 >= n_kt) break;
+      step(I1{}, I2{}, I0{}, i + 1, sb0, sb1, sa0, sa1);
+      if (i + 2 >= n_kt) break;
+      step(I2{}, I3{}, I1{}, i + 2, sa0, sa1, sb0, sb1);
+      if (i + 3 >= n_kt) break;
+      step(I3{}, I0{}, I2{}, i + 3, sb0, sb1, sa0, sa1);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this item's DMA is complete
+    __builtin_amdgcn_s_barrier();                     // and every wavefront is done with the ring
 
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  f32x16 sa0, sa1, sb0, sb1;
-  asm volatile("s_waitcnt vmcnt(4)" ::: "memory");  // tiles 0 and 1 have landed
-  __builtin_amdgcn_s_barrier();
-  qk(I0{}, sa0, sa1);
-  for (int i = 0; i < n_kt; i += 4) {
-    step(I0{}, I1{}, I3{}, i, sa0, sa1, sb0, sb1);
-    if (i + 1 >= n_kt) break;
-    step(I1{}, I2{}, I0{}, i + 1, sb0, sb1, sa0, sa1);
-    if (i + 2 >= n_kt) break;
-    step(I2{}, I3{}, I1{}, i + 2, sa0, sa1, sb0, sb1);
-    if (i + 3 >= n_kt) break;
-    step(I3{}, I0{}, I2{}, i + 3, sb0, sb1, sa0, sa1);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this segment's DMA is complete
-  __builtin_amdgcn_s_barrier();                     // and every wavefront is done with the ring
-
-  const float l_tot = pair_sum(l_run);
-  // The wavefront's 32 result rows (query vector q, 256 bytes each) pass
-  // through its own 8 KB of the now idle V ring, so that every global store
-  // writes four whole rows instead of 16-byte pieces of 32 rows.  In LDS,
-  // 16-byte chunk c of row q sits at position c ^ (q & 15) (conflict-free
-  // writes of the accumulator layout).
-  char* tb = (wave < 2 ? lo_v0 : wave < 4 ? lo_v1 : wave < 6 ? lo_v2 : lo_v3) + (wave & 1) * (32 * kRow);
-  auto put = [&](int c, u32x2 w) {  // chunk c = elements 8c..8c+7 of row q; this lane holds half hi
-    *(u32x2*)(tb + q * kRow + ((c ^ (q & 15)) << 4) + 8 * hi) = w;
-  };
-  auto get = [&](int row, int c) -> u32x4 { return *(const u32x4*)(tb + row * kRow + ((c ^ (row & 15)) << 4)); };
-  // accumulator register r of d-block b holds dim 32b + 8(r/4) + 4hi + r%4
-  if (full) {
-    const float inv = valid ? 1.f / l_tot : 0.f;
+    // Epilogue.  The next item is claimed first; its answer is read after
+    // this item's results are on their way.
+    const AttnArgs A = args();
+    const PlanView pv = plan_view(A.plan, A.n_tiles);
+    int got = 0;
+    if (tid == 0) got = atomicAdd(&pv.hdr[jq], 1);
+    const int lrel = it_field(0), oi = it_field(1), kv = it_field(2);
+    const int layer = A.lb + lrel;
+    const int nsp = pv.nsp[oi];
+    const int piece = min(it_field(3), nsp - 1);  // (a bound, as in start_item)
+    const int64_t m0 = (A.n_tiles - 1 - oi) * RT;
+    const bool valid = g_q >= 0;
+    const int el = lane_id(), eq = el & 31, ehi = el >> 5;
+    const int64_t m = m0 + wave * RW + eq / G;
+    const int h = kv * G + eq % G;
+    const float l_tot = pair_sum(l_run);
+    // The wavefront's 32 result rows (query vector q, 256 bytes each) pass
+    // through 8 KB of ring slots 2 and 3, so that every global store writes
+    // four whole rows instead of 16-byte pieces of 32 rows.  In LDS, 16-byte
+    // chunk c of row q sits at position c ^ (q & 15) (conflict-free writes of
+    // the accumulator layout).
+    char* tb = (wave < 2 ? up_k2 : wave < 4 ? up_k3 : wave < 6 ? lo_v2 : lo_v3) + (wave & 1) * (32 * kRow);
+    auto put = [&](int c, u32x2 w) {  // chunk c = elements 8c..8c+7 of row q; this lane holds half hi
+      *(u32x2*)(tb + eq * kRow + ((c ^ (eq & 15)) << 4) + 8 * ehi) = w;
+    };
+    auto get = [&](int row, int c) -> u32x4 { return *(const u32x4*)(tb + row * kRow + ((c ^ (row & 15)) << 4)); };
+    // accumulator register r of d-block b holds dim 32b + 8(r/4) + 4hi + r%4
+    if (nsp == 1) {
+      const float inv = valid ? 1.f / l_tot : 0.f;
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
+      for (int d = 0; d < 4; ++d)
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        u32x2 w;
-        w[0] = pack_bf16x2(o[d][4 * rq] * inv, o[d][4 * rq + 1] * inv);
-        w[1] = pack_bf16x2(o[d][4 * rq + 2] * inv, o[d][4 * rq + 3] * inv);
-        put(4 * d + rq, w);
+        for (int rq = 0; rq < 4; ++rq) {
+          u32x2 w;
+          w[0] = pack_bf16x2(o[d][4 * rq] * inv, o[d][4 * rq + 1] * inv);
+          w[1] = pack_bf16x2(o[d][4 * rq + 2] * inv, o[d][4 * rq + 3] * inv);
+          put(4 * d + rq, w);
+        }
+      if (valid && A.lse && ehi == 0)
+        A.lse[((int64_t)layer * A.Hq + h) * A.n_sel + m] = (m_use + __log2f(l_tot)) * kLn2;
+      const uint64_t has_row = __ballot(valid);  // bit q: query vector q has an output row
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      // store s covers rows R = 4s .. 4s+3 in output order: head hh = R / RW, selected row j = R % RW
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int R = 4 * s + (el >> 4), c = el & 15;
+        const int hh = R / RW, j = R % RW, qq = j * G + hh;
+        const u32x4 v = get(qq, c);
+        if ((has_row >> qq) & 1)
+          *(u32x4*)(A.out + (((int64_t)layer * A.Hq + kv * G + hh) * A.n_sel + m0 + wave * RW + j) * 128 + 8 * c) = v;
       }
-    if (valid && a.lse && hi == 0)
-      a.lse[((int64_t)layer * a.Hq + h) * a.n_sel + m] = (m_use + __log2f(l_tot)) * kLn2;
-    const uint64_t has_row = __ballot(valid);  // bit q: query vector q has an output row
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    // store s covers rows R = 4s .. 4s+3 in output order: head hh = R / RW, selected row j = R % RW
+    } else {
+      // The piece's output row O / sum, scaled by 2^-e so that its largest
+      // magnitude lies in [0.5, 1), is kept in fp16 (11 significant bits
+      // relative to that element; the scale keeps the bf16 range of V within
+      // fp16's).
+      const int64_t slot = (int64_t)lrel * A.part_cap + pv.ppre[oi] + kv * nsp + piece;  // < part_cap per layer
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      float amax = 0.f;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const int R = 4 * s + (lane >> 4), c = lane & 15;
-      const int hh = R / RW, j = R % RW, qq = j * G + hh;
-      const u32x4 v = get(qq, c);
-      if ((has_row >> qq) & 1)
-        *(u32x4*)(a.out + (((int64_t)layer * a.Hq + kv * G + hh) * a.n_sel + m0 + wave * RW + j) * 128 + 8 * c) = v;
-    }
-  } else {
-    // The piece's output row O / sum, scaled by 2^-e so that its largest
-    // magnitude lies in [0.5, 1), is kept in fp16 (11 significant bits,
-    // finer than the bf16 result; the scale keeps the bf16 range of V within
-    // fp16's).
-    const int64_t slot = (int64_t)lrel * a.part_cap + pv.ppre[oi] + kv * nsp + piece;  // < part_cap per layer
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    float amax = 0.f;
+      for (int d = 0; d < 4; ++d)
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
+        for (int r = 0; r < 16; ++r) amax = fmaxf(amax, fabsf(o[d][r]));
+      amax = pair_max(amax) * inv;
+      const int e = amax > 0.f ? min(max(__builtin_amdgcn_frexp_expf(amax), -100), 100) : 0;  // 2^-e stays normal
+      const float sc_e = inv * __builtin_ldexpf(1.f, -e);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) amax = fmaxf(amax, fabsf(o[d][r]));
-    amax = pair_max(amax) * inv;
-    const int e = amax > 0.f ? min(max(__builtin_amdgcn_frexp_expf(amax), -100), 100) : 0;  // 2^-e stays normal
-    const float sc_e = inv * __builtin_ldexpf(1.f, -e);
+      for (int d = 0; d < 4; ++d)
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const f32x4 v4 = {o[d][4 * rq] * sc_e, o[d][4 * rq + 1] * sc_e, o[d][4 * rq + 2] * sc_e, o[d][4 * rq + 3] * sc_e};
-        put(4 * d + rq, __builtin_bit_cast(u32x2, __builtin_convertvector(v4, f16x4)));
+        for (int rq = 0; rq < 4; ++rq) {
+          const f32x4 v4 = {o[d][4 * rq] * sc_e, o[d][4 * rq + 1] * sc_e, o[d][4 * rq + 2] * sc_e, o[d][4 * rq + 3] * sc_e};
+          put(4 * d + rq, __builtin_bit_cast(u32x2, __builtin_convertvector(v4, f16x4)));
+        }
+      if (ehi == 0) {
+        const f32x4 ml = {m_use, l_tot, (float)e, 0.f};
+        *(f32x4*)(A.part_ml + (slot * kQPerWG + wave * 32 + eq) * 4) = ml;
       }
-    if (hi == 0) {
-      const f32x4 ml = {m_use, l_tot, (float)e, 0.f};
-      *(f32x4*)(a.part_ml + (slot * kQPerWG + wave * 32 + q) * 4) = ml;
-    }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    uint16_t* pp = a.part + (slot * kQPerWG + wave * 32) * 128;  // the wavefront's 32 consecutive rows
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      uint16_t* pp = A.part + (slot * kQPerWG + wave * 32) * 128;  // the wavefront's 32 consecutive rows
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const int R = 4 * s + (lane >> 4), c = lane & 15;
-      *(u32x4*)(pp + R * 128 + 8 * c) = get(R, c);
+      for (int s = 0; s < 8; ++s) {
+        const int R = 4 * s + (el >> 4), c = el & 15;
+        *(u32x4*)(pp + R * 128 + 8 * c) = get(R, c);
+      }
     }
+    // every wavefront is done with ring slots 2 and 3 and with s_it before
+    // the next item is written there
+    __syncthreads();
+    if (!next_item(A, got)) break;
   }
 }
 
@@ -1084,14 +1149,15 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call, int64_
   return p;
 }
 
-// Workgroups of the attention launch and of the combine launch.
+// Workgroups of the attention launch (resident, one per CU, each taking items
+// until the queues are empty; no more than there are items) and of the
+// combine launch.
 static int64_t mfma_grid(const AttnArgs& a) {
   // items per queue and layer: at most one per row tile and KV head of the
   // queue, plus the extra pieces of cut row tiles (bounded by part_cap)
   const int nq = n_queues(a.Hkv);
-  const int64_t per_q = (a.n_tiles * a.Hkv + a.part_cap + nq - 1) / nq;
-  const int64_t share = kXcds / nq;
-  return (per_q * a.layers + share - 1) / share * kXcds;
+  const int64_t items = (a.n_tiles * a.Hkv + a.part_cap + nq - 1) / nq * nq * a.layers;
+  return std::min<int64_t>(kPlanCUs, items);
 }
 static int64_t combine_grid(const AttnArgs& a) {
   // cut row tiles lead the longest-first order, and each fills at least

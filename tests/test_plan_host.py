@@ -79,7 +79,7 @@ def plan(sel, n_sel, RT, T, hkv, part_cap):
         if np_ > 1:
             for j in range(np_):
                 cnt = (pj[j + 1] - pj[j]) // kvq
-                b, e = j * v // np_, (j + 1) * v // np_
+                b, e = j * S, min((j + 1) * S, v)
                 for kvl in range(kvq):
                     pos = pj[j] + kvl * cnt + i
                     assert pos not in desc, f"position {pos} written twice"
