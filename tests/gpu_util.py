@@ -49,3 +49,29 @@ def ulp(x, dtype):
 
 def log(*a):
     print(*a, flush=True)
+
+
+def check_scores_and_selection(got_scores, ref_scores, got_sel, k, cs1, select_top):
+    """Scores: float32, equal to the oracle's or one ulp away (the GPU sums the
+    float64 squares in another order; the two roundings to float32 can land on
+    adjacent values within ~1e-16 of a midpoint).  Selection: identical to the
+    oracle's when the scores are; otherwise exact on the GPU's own scores, and
+    every index in one set but not the other within a relative score gap of
+    1e-6 of its counterpart (the tie window of the selection bar)."""
+    g = np.asarray(got_scores, np.float32)
+    r = np.asarray(ref_scores, np.float32)
+    d = np.abs(g.view(np.int32).astype(np.int64) - r.view(np.int32).astype(np.int64))
+    assert d.max(initial=0) <= 1, f"scores differ by {d.max()} float32 ulps"
+    sel = np.asarray(got_sel[:k], np.int64)
+    want = select_top(r, k, cs1)
+    if not d.any():
+        assert sel.tolist() == want.tolist()
+        return 0
+    assert sel.tolist() == select_top(g, k, cs1).tolist()
+    extra, missing = sorted(set(sel.tolist()) - set(want.tolist())), sorted(set(want.tolist()) - set(sel.tolist()))
+    assert len(extra) == len(missing)
+    sc = r.astype(np.float64)
+    for i, j in zip(extra, missing):
+        a, b = sc[i - cs1], sc[j - cs1]
+        assert abs(a - b) < 1e-6 * max(a, b), (i, j, a, b)
+    return int(d.sum())
