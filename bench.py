@@ -61,6 +61,9 @@ def parse():
                    help="steps also timed with one batched attention call over all layers (0: skip)")
     p.add_argument("--graph-steps", type=int, default=3,
                    help="steps of the per-layer composition captured once into a HIP graph and replayed (0: skip)")
+    p.add_argument("--oracle-full", choices=("none", "tiny", "qwen8k"), default="none",
+                   help="time the CPU oracle's whole composition of a small workload (all layers, "
+                        "no extrapolation) and print one JSON line; needs no GPU")
     p.add_argument("--sweep", choices=("none", "rebase", "attention"), default="none",
                    help="rebase: 8k/65k/262k-token K caches with and without a cache flush, and the "
                         "per-token (scalar re-basing) kernel on the 65k cache; "
@@ -138,8 +141,49 @@ def run_compose(inp, w, rho, binding, torch, out, lse, sel, scores, ws, batched,
     return k
 
 
+def host_info():
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        threads = os.cpu_count()
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
+    return threads, cpu_model
+
+
+def oracle_full(name):
+    """The CPU oracle's whole composition of a small workload (every layer, no
+    extrapolation): re-basing, scoring, selection, and the scatter and attention
+    of every layer, timed after the inputs are built."""
+    import oracle
+    from paper_2607_19547_amd import synth
+    w = synth.WORKLOADS[name]
+    d = oracle.inputs.build(w)
+    args = (w.dtype, w.head_dim, w.sections, w.base, d["chunk_start"], d["chunk_offsets"], d["k_stored"],
+            d["v_stored"], d["q_fresh"], d["k_fresh"], d["v_fresh"], w.rho, w.score_layer)
+    reps = 20 if name == "tiny" else 1
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        oracle.compose.compose(*args)
+        times.append(time.perf_counter() - t0)
+    threads, cpu_model = host_info()
+    print(json.dumps({"oracle_full": {"workload": name, "rho": w.rho, "n_layers": w.n_layers, "n_tokens": w.n_tokens,
+                                      "median_s": float(np.median(times)), "reps": reps, "cores": threads,
+                                      "host_cpus": os.cpu_count(), "cpu_model": cpu_model,
+                                      "kind": "oracle", "dtype": "f64"}}), flush=True)
+
+
 def main():
     args = parse()
+    if args.oracle_full != "none":
+        return oracle_full(args.oracle_full)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the library has no "
               f"multi-GPU path: run with --gpus 1", file=sys.stderr)
@@ -493,20 +537,9 @@ def cpu_baseline(w, rho):
                                  oracle.bf16.decode(vp), sel, w.cs1)
     t_attn = time.perf_counter() - t0
     total_s = w.n_layers * (t_rebase + t_attn) + t_select
-    threads = None
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-    except Exception:
-        threads = os.cpu_count()
+    threads, cpu_model = host_info()
     log(f"[bench] cpu_baseline: rebase/layer {t_rebase:.2f} s, score+select {t_select:.2f} s, "
         f"attention/layer {t_attn:.2f} s -> {total_s:.1f} s per composition (extrapolated)")
-    cpu_model = None
-    try:
-        with open("/proc/cpuinfo") as f:
-            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
-    except OSError:
-        pass
     return dict(value=total_s * 1e3, unit="ms", cores=threads, kind="oracle",
                 host_cpus=os.cpu_count(), cpu_model=cpu_model,
                 sample=(f"1 of {w.n_layers} layers (rebase {t_rebase:.2f} s + scatter/attention "

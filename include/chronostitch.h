@@ -179,8 +179,12 @@ cs_status score_deviation_topk(const cs_geometry* g, const void* k_cache,
  *      the storage dtype, scattered into the cache; V rows are scattered as in
  *      selective_attend_scatter;
  *   2. Q row (every query head): f(q_pre, p'_t), rounded to the storage
- *      dtype, kept in the workspace;
+ *      dtype;
  *   3. attention exactly as in selective_attend_scatter.
+ * For bf16 with head_dim 128 the rotations run inside the attention's own
+ * launches (the keys while they are scattered, the queries as the attention
+ * loads them) from a cos/sin table of the selected tokens kept in the
+ * workspace; otherwise the rotated queries pass through the workspace.
  * The result equals selective_attend_scatter on q_fresh = f(q_pre, p') and
  * k_fresh = f(k_pre, p') rounded the same way.  Angles are formed in float64
  * and reduced modulo 2*pi (float32 cos/sin), as in compose_rebase_k.
@@ -192,8 +196,10 @@ cs_status score_deviation_topk(const cs_geometry* g, const void* k_cache,
  *                  (compose_rebase_k's global_coords, copied to the device)
  *   workspace      DEVICE, >= selective_attend_scatter_rope_workspace() for
  *                  the same n_sel and n_layers_per_call >= layer_end -
- *                  layer_begin: the attention's partials plus the rotated
- *                  queries (n_layers x H_q x n_sel x D elements)
+ *                  layer_begin: the attention's partials plus, for bf16 with
+ *                  head_dim 128, the cos/sin table (n_sel x D/2 x 8 bytes),
+ *                  otherwise the rotated queries (n_layers x H_q x n_sel x D
+ *                  elements)
  *   other arguments as for selective_attend_scatter.
  * Errors: CS_ERR_INVALID_ARGUMENT, CS_ERR_WORKSPACE_TOO_SMALL, CS_ERR_HIP. */
 cs_status selective_attend_scatter_rope_workspace(const cs_geometry* g, int64_t n_sel,

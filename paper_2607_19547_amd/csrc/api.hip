@@ -385,11 +385,14 @@ struct TraceSuppress {
   ~TraceSuppress() { t_trace_suppressed = prev; }
 };
 
-// Workspace of the fused-rotary variant: the attention's, then the rotated
-// queries [layers in call][H_q][n_sel][D].
+// Workspace of the fused-rotary variant: the attention's, then, on the MFMA
+// path (bf16, head_dim 128), the cos/sin table of the selected tokens
+// [n_sel][D/2] float2 (the attention rotates the queries as it loads them),
+// elsewhere the rotated queries [layers in call][H_q][n_sel][D].
 static size_t rope_ws(const Geo& g, const AttnPlan& p, int64_t n_sel, int layers, size_t* att_bytes) {
   const size_t att = p.mfma && n_sel > 0 && layers > 0 ? p.ws_fixed_bytes + p.ws_bytes_per_layer * (size_t)layers : 0;
   *att_bytes = align_up(att, 256);
+  if (p.mfma) return *att_bytes + rope_table_bytes(n_sel);
   return *att_bytes + (size_t)layers * g.Hq * n_sel * g.D * g.esize;
 }
 
@@ -412,18 +415,24 @@ static cs_status attend_scatter_rope(const cs_geometry* gp, const Geo& g, const 
   if (cv.paged && p.mfma && !chunks_tile_aligned(g))
     return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
   hipStream_t s = (hipStream_t)stream;
-  void* q_ws = (char*)workspace + att;
+  void* extra = (char*)workspace + att;  // the cos/sin table (MFMA path) or the rotated queries
+  const RopeJob rope{k_pre, v_fresh, coords, theta.data(), extra};
   for (int pass = 0; pass < 2; ++pass) {  // sizes of every launch first, then the launches
     const bool check = pass == 0;
     if (!check && debug_validate()) {
       st = check_selection(g, sel_idx, n_sel, s);
       if (st) return st;
     }
-    st = launch_rope_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords,
-                             theta.data(), q_ws, s, check);
-    if (!st)
-      st = launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_ws, true, out, lse, workspace, s,
-                            check);
+    if (p.mfma) {  // the rotations run inside the attention's two launches
+      st = launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, q_pre, false, out, lse, workspace, s,
+                            check, nullptr, &rope);
+    } else {
+      st = launch_rope_scatter(g, cv, layer_begin, layer_end, sel_idx, n_sel, q_pre, k_pre, v_fresh, coords,
+                               theta.data(), extra, s, check);
+      if (!st)
+        st = launch_attention(g, p, cv, layer_begin, layer_end, sel_idx, n_sel, extra, true, out, lse, workspace, s,
+                              check);
+    }
     if (st) return st;
   }
   return CS_OK;

@@ -137,6 +137,8 @@ struct AttnArgs {
   int part_cap;      // partial slots per layer
   int q_by_slot;     // q is [layers in call][H_q][n_sel][128] (rows in selection order), else [L][H_q][n][128]
   int desc_off;      // item descriptors in the plan (set by the planning kernel's caller)
+  const float2* rope_tab;  // [n_sel][64] cos/sin of the selected tokens: q holds pre-rotary queries, rotated on
+                           // load; NULL: q is already rotated
   float scale_log2;  // log2(e) / sqrt(D)
 };
 
@@ -490,6 +492,91 @@ __global__ __launch_bounds__(1024) void plan_scatter(const PlanArgs p, const Row
   scatter_body<W>(rows, sa, (int64_t)(blockIdx.x - 1) * 1024 + threadIdx.x, (int64_t)(gridDim.x - 1) * 1024);
 }
 
+// The fused rotary scatter (Eq. 2 at the global coordinates p' of the
+// repair step): a workgroup takes kPrTok selected tokens of one layer, builds
+// their cos/sin table in LDS (angles in float64, reduced modulo 2*pi, rounded
+// to float32, as the re-basing kernels do; the call's first layer also keeps
+// it in the workspace for the attention's queries), rotates their fresh keys
+// into the cache rows and copies their fresh values.  Eight lanes per row,
+// each holding the pairs (8j .. 8j+7) and (64 + 8j .. 64 + 8j+7).
+constexpr int kPrTok = 32;   // selected tokens per workgroup
+constexpr int kPrTabW = 65;  // LDS table row stride (float2): one pad entry spreads the banks
+struct RopeRowsArgs {
+  const uint16_t* k_pre;  // [L][H_kv][n][128]
+  const uint16_t* v_new;  // [L][H_kv][n][128]
+  const int32_t* sel;
+  const int32_t* coords;  // [T][3]
+  float2* tab;            // [n_sel][64]
+  int64_t T, n, n_sel, cs1;
+  int Hkv, lb, nblk;      // nblk: workgroups per layer
+  int sec0, sec01;
+  double theta[64];
+};
+
+template <typename Rows>
+__device__ void rope_rows_body(const RopeRowsArgs& a, const Rows& rows, int blk, int lrel) {
+  __shared__ float2 tab[kPrTok * kPrTabW];
+  __shared__ int tok_of[kPrTok];
+  const int tid = threadIdx.x;
+  const int64_t m0 = (int64_t)blk * kPrTok;
+  const int nm = (int)min<int64_t>(kPrTok, a.n_sel - m0);
+  const int layer = a.lb + lrel;
+  if (tid < kPrTok) {
+    int t = -1;
+    if (tid < nm) {
+      const int64_t g = a.sel[m0 + tid];
+      if (g >= a.cs1 && g < a.T) t = (int)g;  // out-of-contract index: the row is skipped
+    }
+    tok_of[tid] = t;
+  }
+  __syncthreads();
+  for (int e = tid; e < kPrTok * 64; e += 1024) {
+    const int r = e >> 6, i = e & 63;
+    const int t = tok_of[r];
+    float2 cs = make_float2(1.f, 0.f);
+    if (t >= 0) cs = cos_sin_of((double)a.coords[(int64_t)t * 3 + axis_of(i, a.sec0, a.sec01)] * a.theta[i]);
+    tab[r * kPrTabW + i] = cs;
+    if (lrel == 0 && r < nm) a.tab[(m0 + r) * 64 + i] = cs;
+  }
+  __syncthreads();
+  const int j = tid & 7;
+  const int total = kPrTok * 2 * a.Hkv;  // rows: K of each KV head (rotated), then V (copied)
+  for (int idx = tid >> 3; idx < total; idx += 128) {
+    const int r = idx % kPrTok, kind = idx / kPrTok;
+    const int t = tok_of[r];
+    if (t < 0) continue;
+    const bool is_k = kind < a.Hkv;
+    const int h = is_k ? kind : kind - a.Hkv;
+    const uint16_t* src = (is_k ? a.k_pre : a.v_new) + (((int64_t)layer * a.Hkv + h) * a.n + (t - a.cs1)) * 128;
+    uint16_t* dst = (uint16_t*)rows.row(!is_k, (int64_t)layer * a.Hkv + h, t, 256);
+    u32x4 wa = *(const u32x4*)(src + 8 * j), wb = *(const u32x4*)(src + 64 + 8 * j);
+    if (is_k) {
+      float c[8], sn[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float2 v = tab[r * kPrTabW + 8 * j + e];
+        c[e] = v.x;
+        sn[e] = v.y;
+      }
+      rotate8(wa, wb, c, sn);
+    }
+    *(u32x4*)(dst + 8 * j) = wa;
+    *(u32x4*)(dst + 64 + 8 * j) = wb;
+  }
+}
+
+// The plan (workgroup 0) and the fused rotary scatter of the call's fresh rows
+// (the other workgroups: layer (b - 1) / nblk, tokens of block (b - 1) % nblk).
+template <typename Rows>
+__global__ __launch_bounds__(1024) void plan_rope_scatter(const PlanArgs p, const Rows rows, const RopeRowsArgs ra) {
+  if (blockIdx.x == 0) {
+    plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.desc_off, p.plan);
+    return;
+  }
+  const int b = blockIdx.x - 1;
+  rope_rows_body(ra, rows, b % ra.nblk, b / ra.nblk);
+}
+
 template <int G, typename Rows>
 __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, const Rows rows) {
   constexpr bool kPaged = !std::is_same<Rows, FlatRows>::value;
@@ -699,6 +786,26 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
         const uint16_t* qp = A.q + qrow * 128 + 8 * (ln >> 5);
 #pragma unroll
         for (int s = 0; s < 8; ++s) qb[s] = *(const bf16x8*)(qp + 16 * s);
+        if (A.rope_tab) {
+          // pre-rotary query: qb[s] and qb[s + 4] hold elements d and d + 64
+          // of the same rotary pairs (d = 16s + 8hi + x), rotated here with the
+          // selected token's cos/sin (Eq. 2 at p') and rounded to bf16
+          const float2* tb = A.rope_tab + m * 64 + 8 * (ln >> 5);
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+            float c[8], sn[8];
+#pragma unroll
+            for (int x = 0; x < 8; ++x) {
+              const float2 v = tb[16 * s + x];
+              c[x] = v.x;
+              sn[x] = v.y;
+            }
+            u32x4 wa = __builtin_bit_cast(u32x4, qb[s]), wb = __builtin_bit_cast(u32x4, qb[s + 4]);
+            rotate8(wa, wb, c, sn);
+            qb[s] = __builtin_bit_cast(bf16x8, wa);
+            qb[s + 4] = __builtin_bit_cast(bf16x8, wb);
+          }
+        }
       } else {
 #pragma unroll
         for (int s = 0; s < 8; ++s) qb[s] = bf16x8{};
@@ -1170,9 +1277,11 @@ static int64_t plan_scatter_blocks(const ScatterArgs& sa) {
 }
 
 template <int G, typename Rows>
-static void launch_mfma_g(const AttnArgs& a, const Rows& rows, const ScatterArgs* sa, hipStream_t s) {
+static void launch_mfma_g(const AttnArgs& a, const Rows& rows, const ScatterArgs* sa, const RopeRowsArgs* ra,
+                          hipStream_t s) {
   static_assert(sizeof(AttnArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
   static_assert(sizeof(PlanArgs) + sizeof(Rows) + sizeof(ScatterArgs) <= 4096, "kernel arguments within 4 KB");
+  static_assert(sizeof(PlanArgs) + sizeof(Rows) + sizeof(RopeRowsArgs) <= 4096, "kernel arguments within 4 KB");
   PlanArgs pa;
   pa.sel = a.sel;
   pa.n_sel = a.n_sel;
@@ -1184,7 +1293,11 @@ static void launch_mfma_g(const AttnArgs& a, const Rows& rows, const ScatterArgs
   pa.part_cap = a.part_cap;
   pa.desc_off = a.desc_off;
   pa.plan = a.plan;
-  if (sa) {
+  if (ra) {
+    TraceScope tr("plan_rope_scatter", s);
+    const unsigned blocks = (unsigned)(1 + (int64_t)ra->nblk * a.layers);
+    hipLaunchKernelGGL(plan_rope_scatter<Rows>, dim3(blocks), dim3(1024), 0, s, pa, rows, *ra);
+  } else if (sa) {
     TraceScope tr("plan_scatter", s);
     const unsigned blocks = (unsigned)plan_scatter_blocks(*sa);
     if (scatter_word(*sa) == 16)
@@ -1206,14 +1319,15 @@ static void launch_mfma_g(const AttnArgs& a, const Rows& rows, const ScatterArgs
 }
 
 template <typename Rows>
-static cs_status launch_mfma(int G, const AttnArgs& a, const Rows& rows, const ScatterArgs* sa, hipStream_t s) {
+static cs_status launch_mfma(int G, const AttnArgs& a, const Rows& rows, const ScatterArgs* sa,
+                             const RopeRowsArgs* ra, hipStream_t s) {
   switch (G) {
-    case 1: launch_mfma_g<1>(a, rows, sa, s); break;
-    case 2: launch_mfma_g<2>(a, rows, sa, s); break;
-    case 4: launch_mfma_g<4>(a, rows, sa, s); break;
-    case 8: launch_mfma_g<8>(a, rows, sa, s); break;
-    case 16: launch_mfma_g<16>(a, rows, sa, s); break;
-    case 32: launch_mfma_g<32>(a, rows, sa, s); break;
+    case 1: launch_mfma_g<1>(a, rows, sa, ra, s); break;
+    case 2: launch_mfma_g<2>(a, rows, sa, ra, s); break;
+    case 4: launch_mfma_g<4>(a, rows, sa, ra, s); break;
+    case 8: launch_mfma_g<8>(a, rows, sa, ra, s); break;
+    case 16: launch_mfma_g<16>(a, rows, sa, ra, s); break;
+    case 32: launch_mfma_g<32>(a, rows, sa, ra, s); break;
     default: return fail(CS_ERR_UNSUPPORTED, "MFMA attention needs H_q/H_kv dividing 32");
   }
   return CS_OK;
@@ -1232,6 +1346,8 @@ static void launch_generic(const Geo& g, const GenAttnArgs& a, const Rows& rows,
                        rows);
 }
 
+size_t rope_table_bytes(int64_t n_sel) { return ((size_t)n_sel * 64 * sizeof(float2) + 255) / 256 * 256; }
+
 bool chunks_tile_aligned(const Geo& g) {
   for (int c = 0; c < g.N; ++c)
     if (g.cs[c] % kKT) return false;
@@ -1240,10 +1356,28 @@ bool chunks_tile_aligned(const Geo& g) {
 
 cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv, int lb, int le,
                            const int32_t* sel, int64_t n_sel, const void* qf, bool q_by_slot, void* out, float* lse,
-                           void* ws, hipStream_t s, bool check_only, const ScatterJob* job) {
+                           void* ws, hipStream_t s, bool check_only, const ScatterJob* job, const RopeJob* rope) {
   const int layers = le - lb;
   ScatterArgs sa;
   if (job) sa = scatter_args(g, lb, le, sel, n_sel, job->kf, job->vf);
+  RopeRowsArgs ra;
+  if (rope) {  // (MFMA path only: bf16, head_dim 128)
+    ra.k_pre = (const uint16_t*)rope->k_pre;
+    ra.v_new = (const uint16_t*)rope->v_new;
+    ra.sel = sel;
+    ra.coords = rope->coords;
+    ra.tab = (float2*)rope->tab;
+    ra.T = g.T;
+    ra.n = g.n;
+    ra.n_sel = n_sel;
+    ra.cs1 = g.cs1;
+    ra.Hkv = g.Hkv;
+    ra.lb = lb;
+    ra.nblk = (int)((n_sel + kPrTok - 1) / kPrTok);
+    ra.sec0 = g.sec[0];
+    ra.sec01 = g.sec[0] + g.sec[1];
+    for (int i = 0; i < 64; ++i) ra.theta[i] = rope->theta[i];
+  }
   if (p.mfma) {
     if (cv.paged && !chunks_tile_aligned(g))
       return fail(CS_ERR_UNSUPPORTED, "a paged cache needs chunk starts that are multiples of 64 on the MFMA path");
@@ -1267,13 +1401,16 @@ cs_status launch_attention(const Geo& g, const AttnPlan& p, const CacheView& cv,
     a.part_cap = p.part_cap;
     a.q_by_slot = q_by_slot ? 1 : 0;
     a.desc_off = p.desc_off;
+    a.rope_tab = rope ? (const float2*)rope->tab : nullptr;
     a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g.D));
     cs_status stg = check_grid(mfma_grid(a), 1, 1, kThreads, "selective attention");
+    if (!stg && rope) stg = check_grid(1 + (int64_t)ra.nblk * layers, 1, 1, 1024, "rotary scatter");
     if (!stg && a.part_cap > 0) stg = check_grid(combine_grid(a), layers, 1, 256, "partial combine");
     if (stg || check_only) return stg;
     const ScatterArgs* sp = job ? &sa : nullptr;
-    const cs_status st = cv.paged ? launch_mfma(g.G, a, cv.pages<kMaxPages>(g), sp, s)
-                                  : launch_mfma(g.G, a, cv.flat(g), sp, s);
+    const RopeRowsArgs* rp = rope ? &ra : nullptr;
+    const cs_status st = cv.paged ? launch_mfma(g.G, a, cv.pages<kMaxPages>(g), sp, rp, s)
+                                  : launch_mfma(g.G, a, cv.flat(g), sp, rp, s);
     if (st) return st;
     return check_launch("selective attention launch");
   }

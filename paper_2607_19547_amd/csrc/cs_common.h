@@ -238,10 +238,22 @@ struct ScatterJob {
   const void* kf;
   const void* vf;
 };
+// The rotary embedding of the recomputed rows, fused into the attention
+// launches (bf16, head_dim 128): the scatter rotates the fresh keys at the
+// global coordinates and the attention rotates the queries as it loads them,
+// both from a cos/sin table of the selected tokens built once per call.
+struct RopeJob {
+  const void* k_pre;      // [L][H_kv][n][D] pre-rotary fresh keys
+  const void* v_new;      // [L][H_kv][n][D] fresh values
+  const int32_t* coords;  // DEVICE [T][3] global coordinates
+  const double* theta;    // HOST [D/2]
+  void* tab;              // DEVICE [n_sel][D/2] float2 (cos, sin), workspace
+};
+size_t rope_table_bytes(int64_t n_sel);
 cs_status launch_attention(const Geo& g, const AttnPlan& plan, const CacheView& cv,
                            int lb, int le, const int32_t* sel, int64_t n_sel, const void* qf,
                            bool q_by_slot, void* out, float* lse, void* ws, hipStream_t s, bool check_only = false,
-                           const ScatterJob* job = nullptr);
+                           const ScatterJob* job = nullptr, const RopeJob* rope = nullptr);
 cs_status launch_rope_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,
                               const void* q_pre, const void* k_pre, const void* v_new, const int32_t* coords,
                               const double* theta, void* q_ws, hipStream_t s, bool check_only = false);

@@ -158,8 +158,12 @@ def test_fused_rope_argument_errors_and_workspace(built_lib):
                     workspace=small, stream=0)
     assert code == b.CS_ERR_WORKSPACE_TOO_SMALL
     q = b.Geo(36, 16, 2, 128, (16, 24, 24), "bf16", np.arange(33) * 2048)
+    # bf16 / head_dim 128: the attention's workspace plus a cos/sin table of the selected tokens (64 pairs x 8 B),
+    # the same for any number of layers per call
     assert (b.selective_attend_scatter_rope_workspace(q, 6349, 1)
-            >= b.selective_attend_scatter_workspace(q, 6349, 1) + 16 * 6349 * 128 * 2)
+            >= b.selective_attend_scatter_workspace(q, 6349, 1) + 6349 * 64 * 8)
+    assert (b.selective_attend_scatter_rope_workspace(q, 6349, 1)
+            < b.selective_attend_scatter_workspace(q, 6349, 1) + 6349 * 64 * 8 + 512)
     b.selective_attend_scatter_rope(g, None, None, 0, 1, None, 0, None, None, None, None, None, stream=0)  # nothing to do
 
 
