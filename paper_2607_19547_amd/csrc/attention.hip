@@ -304,6 +304,7 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   // the arrays the plan reads back live in LDS when they fit (global memory
   // otherwise); nsp is also written to the plan for the attention kernels
   __shared__ int l_nu[kPlanLdsTiles], l_nsp[kPlanLdsTiles], l_pj[kPlanLdsPieces];
+  __shared__ int4 l_desc[kPlanSortCap];  // the reordered tail's descriptors (earlier, the piece counts)
   const PlanView pv = plan_view(plan, n_tiles);
   const bool in_lds = n_tiles <= kPlanLdsTiles;
   int* const nu = in_lds ? l_nu : pv.nu;
@@ -339,23 +340,30 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   const int S0 = (int)max<int64_t>(kMinPiece, ((int64_t)W1 * Hkv + per - 1) / per);
   int S = nmax;
   if (S0 < nmax) {
-    const int step = max(1, S0 / 8);
-    for (int k = 0; k < 64; ++k) {
-      const int Sk = S0 + k * step;
-      if (Sk >= nmax) break;
-      int loc = 0;
-      for (int64_t i = tid; i < n_tiles; i += 1024) {
-        const int v = nu[i];
-        if (v > Sk) loc += (v + Sk - 1) / Sk;
-      }
-      if ((int64_t)block_reduce(loc, false, red) * Hkv <= part_cap) {
-        S = Sk;
-        break;
+    // the cut row tiles fill at most ceil(W1 / S0) + n_tiles slots per KV
+    // head; when that fits, so does the exact count below, which then
+    // settles on S0 at once
+    if (((W1 + (int64_t)S0 - 1) / S0 + n_tiles) * Hkv <= part_cap) {
+      S = S0;
+    } else {
+      const int step = max(1, S0 / 8);
+      for (int k = 0; k < 64; ++k) {
+        const int Sk = S0 + k * step;
+        if (Sk >= nmax) break;
+        int loc = 0;
+        for (int64_t i = tid; i < n_tiles; i += 1024) {
+          const int v = nu[i];
+          if (v > Sk) loc += (v + Sk - 1) / Sk;
+        }
+        if ((int64_t)block_reduce(loc, false, red) * Hkv <= part_cap) {
+          S = Sk;
+          break;
+        }
       }
     }
   }
-  // pieces per row tile, partial slots of the cut ones
-  int cut = 0, npmax = 1;
+  // pieces per row tile (non-increasing along the longest-first order, as
+  // n_i is), partial slots of the cut ones
   if (tid == 0) s_base = 0;
   __syncthreads();
   for (int64_t b = 0; b < n_tiles; b += 1024) {
@@ -366,36 +374,32 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
       np = v > S ? (v + S - 1) / S : 1;
       nsp[i] = np;
       if (in_lds) pv.nsp[i] = np;
-      cut += np > 1;
-      npmax = max(npmax, np);
     }
     const int inc = block_scan(np > 1 ? np * Hkv : 0, wsum, &s_base);
     if (i < n_tiles) pv.ppre[i + 1] = inc;
   }
-  const int n_cut = block_reduce(cut, false, red);
-  const int np_max = block_reduce(npmax, true, red);
-  // queue positions of piece j: (cut row tiles with more than j pieces) x KV heads per queue
+  // (block_scan ends on a barrier: every nsp is written)  Most pieces:
+  // nsp[0].  cnt_j, the cut row tiles with more than max(j, 1) pieces, is
+  // where nsp drops to max(j, 1) or below: the row tile before each drop
+  // writes the counts of the j it passes (every j in [1, nj) exactly once).
+  // The counts live in l_desc's LDS until the descriptors are placed.
+  int* const l_cnt = (int*)l_desc;
+  const int np_max = nsp[0];
+  const int nj = np_max > 1 ? np_max : 0;
+  for (int64_t i = tid; i < n_tiles; i += 1024) {
+    const int a = nsp[i], a_next = i + 1 < n_tiles ? nsp[i + 1] : 1;
+    for (int j = max(a_next, 1); j < a; ++j) l_cnt[j] = (int)(i + 1);
+  }
+  // queue positions of piece j: pj[j] = (cnt_0 + ... + cnt_{j-1}) x KV heads per queue
   const int nq = n_queues(Hkv), kvq = Hkv / nq;
   if (tid == 0) s_base = 0;
   __syncthreads();
-  const int nj = np_max > 1 ? np_max : 0;
   for (int b = 0; b < nj; b += 1024) {
     const int j = b + tid;
-    int c = 0;
-    if (j < nj) {
-      // nsp does not increase along the longest-first order: count by bisection
-      const int need = max(j, 1);  // cut row tiles (nsp > 1) with nsp > j
-      int lo = 0, up = (int)n_tiles;  // first index with nsp <= need
-      while (lo < up) {
-        const int mid = (lo + up) >> 1;
-        if (nsp[mid] > need) lo = mid + 1;
-        else up = mid;
-      }
-      c = lo;
-    }
-    const int inc = block_scan(c * kvq, wsum, &s_base);
+    const int inc = block_scan(j < nj ? l_cnt[max(j, 1)] * kvq : 0, wsum, &s_base);
     if (j < nj) pv.pj[j + 1] = l_pj[j + 1] = inc;
   }
+  const int n_cut = nj > 1 ? l_cnt[1] : 0;  // (read before l_desc takes descriptors)
   if (tid == 0) {
     const int per_q = s_base + (int)(n_tiles - n_cut) * kvq;
     pv.ppre[0] = 0;
@@ -411,35 +415,40 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   // Item descriptors, one per queue position (the same in every queue and
   // layer): {row tile, KV head in the queue | piece << 16, first and last key
   // tile of the piece}.  Cut row tiles are a prefix of the longest-first order,
-  // so piece j of row tile i sits at pj[j] + kvl * cnt_j + i.  The last
-  // quarter of the queue (the part handed out by the atomic counters) is
+  // so piece j of row tile i sits at pj[j] + kvl * cnt_j + i; uncut row tile i
+  // at pj[nj] + kvl * (uncut count) + i - (cut count).  One thread per
+  // position.  The last quarter of the queue (the part handed out last) is
   // reordered longest first, so the launch ends on its shortest items; the
   // order of equal lengths is immaterial (an item's descriptor alone fixes
   // its work and its output slots).
-  __shared__ int4 l_desc[kPlanSortCap];
   __shared__ int l_bkt[256];
   if (tid < 256) l_bkt[tid] = 0;
   __syncthreads();
   int4* desc = (int4*)(plan + desc_off);
-  const int p_end = l_pj[nj];
+  const int p_end = s_base;
   const int nun = (int)(n_tiles - n_cut);
-  const int per_q_all = s_base + nun * kvq;
+  const int per_q_all = p_end + nun * kvq;
   const int r0 = per_q_all - (per_q_all + 3) / 4;
   const bool sort_tail = per_q_all - r0 <= kPlanSortCap;
   auto put = [&](int pos, int4 d) {
     if (sort_tail && pos >= r0) l_desc[pos - r0] = d;
     else desc[pos] = d;
   };
-  for (int64_t i = tid; i < n_tiles; i += 1024) {
-    const int v = nu[i], np = nsp[i];
-    if (np > 1) {
-      for (int j = 0; j < np; ++j) {
-        const int cnt = (l_pj[j + 1] - l_pj[j]) / kvq;
-        const int b = j * S, e = min((j + 1) * S, v);  // the same key range for piece j of every row tile
-        for (int kvl = 0; kvl < kvq; ++kvl) put(l_pj[j] + kvl * cnt + (int)i, make_int4((int)i, kvl | (j << 16), b, e));
+  for (int pos = tid; pos < per_q_all; pos += 1024) {
+    if (pos < p_end) {
+      int lo = 0, up = nj;  // piece j: the last section starting at or before pos
+      while (up - lo > 1) {
+        const int mid = (lo + up) >> 1;
+        if (l_pj[mid] <= pos) lo = mid;
+        else up = mid;
       }
+      const int cnt = (l_pj[lo + 1] - l_pj[lo]) / kvq;
+      const int r = pos - l_pj[lo], kvl = r / cnt, i = r - kvl * cnt;
+      const int b = lo * S, e = min((lo + 1) * S, nu[i]);  // the same key range for piece j of every row tile
+      put(pos, make_int4(i, kvl | (lo << 16), b, e));
     } else {
-      for (int kvl = 0; kvl < kvq; ++kvl) put(p_end + kvl * nun + (int)(i - n_cut), make_int4((int)i, kvl, 0, v));
+      const int r = pos - p_end, kvl = r / nun, i = n_cut + (r - kvl * nun);
+      put(pos, make_int4(i, kvl, 0, nu[i]));
     }
   }
   if (!sort_tail) return;  // (uniform)

@@ -192,6 +192,46 @@ def test_constant_values_give_that_value(rho, paged):
     assert bool(torch.isfinite(lse).all())
 
 
+def test_zero_query_many_pieces():
+    """Row tiles cut into many key pieces: 301,056 tokens, 32 query heads on
+    one KV head, 40 selected rows near the end (five row tiles of ~4,700 key
+    tiles, cut into 74 pieces of 64 tiles).  Zero query: lse = ln(t + 1) and
+    the output is the mean of V[0..t] after the merge of every piece."""
+    b = B()
+    hq, hkv, nch = 32, 1, 147
+    cs = np.arange(nch + 1, dtype=np.int64) * CH
+    geo = b.Geo(1, hq, hkv, D, (16, 24, 24), "bf16", cs)
+    T, cs1 = int(cs[-1]), CH
+    n = T - cs1
+    rng = np.random.default_rng(21)
+    sel = np.sort(rng.choice(np.arange(T - 20000, T), size=40, replace=False)).astype(np.int64)
+    log(f"case zero query, many pieces: T={T} k={len(sel)}")
+    K, V = _randn((1, hkv, T, D), 31), _randn((1, hkv, T, D), 32)
+    KF, VF = _randn((1, hkv, n, D), 33), _randn((1, hkv, n, D), 34)
+    Q = torch.zeros((1, hq, n, D), dtype=torch.bfloat16, device="cuda")
+    mean, _ = _post_scatter_mean(_host(V), _host(VF), sel, cs1)
+    S = torch.from_numpy(sel.astype(np.int32)).cuda()
+    k = len(sel)
+    out = torch.empty((1, hq, k, D), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((1, hq, k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(b.selective_attend_scatter_workspace(geo, k, 1), dtype=torch.uint8, device="cuda")
+    b.selective_attend_scatter(geo, K, V, 0, 1, S, k, Q, KF, VF, out, lse, ws)
+    torch.cuda.synchronize()
+    most = int(ws[:64].view(torch.int32)[11])  # the plan's header: most pieces of a row tile
+    log(f"  most pieces of a row tile: {most}")
+    assert most == 74
+    want = torch.from_numpy(np.log(sel + 1.0)).cuda()
+    lerr = float((lse.double() - want[None, None, :]).abs().max())
+    log(f"  lse vs ln(t+1): max abs {lerr:.2e}")
+    assert lerr <= 1e-5
+    exp = torch.from_numpy(mean).cuda()[:, :, None]                          # [1][1][1][k][D]
+    _, e = torch.frexp(exp.abs())
+    tol = torch.ldexp(torch.ones_like(exp), (e - 8).clamp(min=-133)) + PIECE_ABS
+    err = (out.view(1, hkv, hq, k, D).double() - exp).abs()
+    log(f"  output vs mean of V[0..t]: max abs err {float(err.max()):.2e}, max err/tol {float((err / tol).max()):.3f}")
+    assert int((err > tol).sum()) == 0
+
+
 # ------------------------------------------------------------ full-size bit identity
 def test_batched_and_graph_equal_per_layer_36_layers():
     """The timed composition's attention stage at full size (36 layers): one
