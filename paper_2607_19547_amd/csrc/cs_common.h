@@ -112,6 +112,44 @@ __device__ __forceinline__ void rotate8(u32x4& wa, u32x4& wb, const float* c, co
   }
 }
 
+// Row-contiguous lane layout: 16 lanes per 256-byte row, lane jj holding
+// bytes 16 jj .. 16 jj + 15 (elements 8 jj .. 8 jj + 7); pair (i, i + 64) lies
+// in lanes jj and jj ^ 8 of the same row, which swap their words through DPP
+// (row_ror:8 within each 16-lane row).  The rotation is rotate8's arithmetic:
+// first half a' = a c - b s, second half b' = a s + b c.  Every lane of a
+// row must execute this (both halves of a pair are active or neither).
+struct RowRot {
+  float m1[8], m2[8];  // first half: (cos, sin); second half: (sin, cos)
+  bool first;
+};
+__device__ __forceinline__ RowRot row_rot(const float2* tab, int jj) {
+  RowRot r;
+  r.first = jj < 8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float2 t = tab[8 * (jj & 7) + e];
+    r.m1[e] = r.first ? t.x : t.y;
+    r.m2[e] = r.first ? t.y : t.x;
+  }
+  return r;
+}
+__device__ __forceinline__ u32x4 rotate_row16(u32x4 x, const RowRot& r) {
+  u32x4 y;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) y[w] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x[w], 0x128, 0xf, 0xf, false);
+  u32x4 o;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float x0 = bf16_lo(x[w]), x1 = bf16_hi(x[w]), y0 = bf16_lo(y[w]), y1 = bf16_hi(y[w]);
+    // first half: fma(a, c, -(b s)) with a = own, b = partner; second: fma(a, s, b c) with a = partner, b = own
+    const float u0 = r.first ? x0 : y0, v0 = r.first ? y0 : x0, u1 = r.first ? x1 : y1, v1 = r.first ? y1 : x1;
+    const float n0 = r.first ? fmaf(u0, r.m1[2 * w], -(v0 * r.m2[2 * w])) : fmaf(u0, r.m1[2 * w], v0 * r.m2[2 * w]);
+    const float n1 = r.first ? fmaf(u1, r.m1[2 * w + 1], -(v1 * r.m2[2 * w + 1])) : fmaf(u1, r.m1[2 * w + 1], v1 * r.m2[2 * w + 1]);
+    o[w] = pack_bf16x2(n0, n1);
+  }
+  return o;
+}
+
 // ------------------------------------------------------------------ cache row addressing
 // A contiguous cache is one buffer per tensor, [L][H_kv][T][D].  A paged
 // cache keeps chunk c in buffers of its own, [L][H_kv][len_c][D] with
