@@ -215,10 +215,15 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_bu
 constexpr int kPlanHdr = 16;    // header ints, see PlanView
 constexpr int kPlanCUs = 256;   // CU count S is derived from (a constant: results do not depend on the device)
 constexpr int kItemsPerCU = 6;  // target items per CU when row tiles must be cut
-constexpr int kMinPiece = 64;   // smallest piece: 64 key tiles (an item's fixed cost is ~7 tiles)
+// Smallest piece: 16 key tiles.  Short caches and small rho leave few items
+// per CU, and a launch then lasts as long as its longest item (measured: the
+// 8,192-token composition at rho = 0.1 takes 3.04 ms with 16, 4.77 ms with
+// 64; the 65,536-token one, whose pieces are ~137 tiles, is unchanged).
+constexpr int kMinPiece = 16;
 constexpr int kPartCap = 2560;  // partial slots per layer, at most
 constexpr int kPlanLdsTiles = 4096;  // row tiles whose plan arrays the planning workgroup keeps in LDS
-constexpr int kPlanLdsPieces = 2049; // most pieces of a row tile (T < 2^23: ceil(ceil(T / 64) / kMinPiece) <= 2048), + 1
+constexpr int kMaxPieces = 2048;     // most pieces of a row tile (the piece size is raised to keep to it)
+constexpr int kPlanLdsPieces = kMaxPieces + 1;
 constexpr int kPlanSortCap = 2048;   // longest tail (a quarter of a queue) the plan reorders
 constexpr int kXcds = 8;
 
@@ -337,7 +342,7 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   // piece size: about kItemsPerCU items per CU, raised until the partial
   // slots fit in part_cap (no cut at all always fits)
   const int64_t per = (int64_t)kPlanCUs * kItemsPerCU;
-  const int S0 = (int)max<int64_t>(kMinPiece, ((int64_t)W1 * Hkv + per - 1) / per);
+  const int S0 = (int)max<int64_t>(max(kMinPiece, (nmax + kMaxPieces - 1) / kMaxPieces), ((int64_t)W1 * Hkv + per - 1) / per);
   int S = nmax;
   if (S0 < nmax) {
     // the cut row tiles fill at most ceil(W1 / S0) + n_tiles slots per KV
@@ -1243,7 +1248,7 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call, int64_
   // Partial slots: a piece has at least kMinPiece key tiles, so a row tile
   // has at most ceil(ceil(T / 64) / kMinPiece) pieces; the plan keeps the
   // total under kPartCap per layer by enlarging the pieces.
-  const int64_t max_pieces = ((g.T + kKT - 1) / kKT + kMinPiece - 1) / kMinPiece;
+  const int64_t max_pieces = std::min<int64_t>(kMaxPieces, ((g.T + kKT - 1) / kKT + kMinPiece - 1) / kMinPiece);
   // the plan counts key tiles of a layer, and items of a call, in 32-bit integers
   if (p.n_tiles * ((g.T + kKT - 1) / kKT) * g.Hkv >= (int64_t(1) << 31) ||
       p.n_tiles * g.Hkv * std::max<int64_t>(1, max_pieces) * std::max(1, layers_per_call) >= (int64_t(1) << 31)) {

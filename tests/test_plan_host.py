@@ -11,7 +11,7 @@ import math
 import numpy as np
 import pytest
 
-KT, CUS, ITEMS_PER_CU, MIN_PIECE, XCDS = 64, 256, 6, 64, 8
+KT, CUS, ITEMS_PER_CU, MIN_PIECE, MAX_PIECES, XCDS = 64, 256, 6, 16, 2048, 8
 
 
 def n_queues(hkv):
@@ -19,7 +19,7 @@ def n_queues(hkv):
 
 
 def part_cap_of(n_tiles, T, hkv, cap=2560):
-    max_pieces = ((T + KT - 1) // KT + MIN_PIECE - 1) // MIN_PIECE
+    max_pieces = min(MAX_PIECES, ((T + KT - 1) // KT + MIN_PIECE - 1) // MIN_PIECE)
     pc = min(cap, n_tiles * hkv * (max_pieces if max_pieces > 1 else 0))
     return 0 if pc < 2 * hkv else pc
 
@@ -38,7 +38,7 @@ def plan(sel, n_sel, RT, T, hkv, part_cap):
     nu = nu_t[::-1]                     # longest-first order i = n_tiles - 1 - t
     W1, nmax = sum(nu), max(nu)
     per = CUS * ITEMS_PER_CU
-    S0 = max(MIN_PIECE, -(-(W1 * hkv) // per))
+    S0 = max(MIN_PIECE, -(-nmax // MAX_PIECES), -(-(W1 * hkv) // per))
     S = nmax
     if S0 < nmax:
         step = max(1, S0 // 8)
@@ -104,6 +104,7 @@ def check(sel, n_sel, G, T, hkv, part_cap=None):
     assert p["per_q"] <= per_q_bound
     assert p["ppre"][-1] <= part_cap, "partial slots within the per-layer count"
     assert all(a >= b for a, b in zip(p["nsp"], p["nsp"][1:])), "pieces non-increasing (cut row tiles lead)"
+    assert max(p["nsp"]) <= MAX_PIECES, "the planning workgroup keeps at most MAX_PIECES sections"
     pieces = {}
     for (i, kvl, j, b, e) in p["desc"].values():
         assert 0 <= i < n_tiles and 0 <= kvl < hkv // nq and 0 <= j < p["nsp"][i]
@@ -121,7 +122,7 @@ def check(sel, n_sel, G, T, hkv, part_cap=None):
 
 
 GEOS = [(8, 2, 65536, 6349), (8, 2, 8192, 615), (1, 1, 30000, 4000), (4, 8, 4096, 900), (32, 16, 9000, 333),
-        (2, 3, 20000, 2500), (16, 4, 65536, 61000)]
+        (2, 3, 20000, 2500), (16, 4, 65536, 61000), (32, 1, 301056, 40)]
 
 
 @pytest.mark.parametrize("G,hkv,T,k", GEOS)
