@@ -211,7 +211,7 @@ def main():
         other = bench_rho(inp, w, rho, args.batched_steps, 1, binding, torch, not args.batched_layers)
     fused = None
     if args.fused_rope_steps > 0:
-        fused = bench_rho(inp, w, rho, args.fused_rope_steps, 1, binding, torch, False, fused=True)
+        fused = bench_fused_vs_plain(inp, w, rho, args.fused_rope_steps, binding, torch)
     paged = None
     if args.paged_steps > 0:
         paged = bench_rho(inp, w, rho, args.paged_steps, 1, binding, torch, False, paged=True)
@@ -242,6 +242,47 @@ def gemm_context(torch, m=8192, n=8192, k=16384, reps=10):
     log(f"[bench] vendor bf16 GEMM {m}x{n}x{k}: {ms:.3f} ms, {tf:.1f} TFLOP/s")
     del a, b, c
     return dict(shape=[m, n, k], ms=round(ms, 4), TFLOPs=round(tf, 1))
+
+
+def bench_fused_vs_plain(inp, w, rho, steps, binding, torch):
+    """The fused-RoPE composition and the plain one in alternating steps (plain, fused, plain, ...), so
+    that the clock's drift over a run (it follows power and temperature) weighs on both alike; medians
+    of each."""
+    b = binding
+    n = w.n_candidates
+    scores = torch.empty(n, dtype=torch.float32, device="cuda")
+    sel = torch.empty(n, dtype=torch.int32, device="cuda")
+    k = b.score_deviation_topk(inp.geo, inp.K, w.score_layer, inp.KF[w.score_layer], rho, scores, sel)
+    out = torch.empty((w.n_layers, w.n_q_heads, k, w.head_dim), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((w.n_layers, w.n_q_heads, k), dtype=torch.float32, device="cuda")
+    ws_f = torch.empty(max(b.selective_attend_scatter_rope_workspace(inp.geo, k, 1), 1), dtype=torch.uint8,
+                       device="cuda")
+    ws_p = torch.empty(max(b.selective_attend_scatter_workspace(inp.geo, k, 1), 1), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    log(f"[bench] rho={rho}: n_sel={k}, fused RoPE and plain in alternating steps, steps {steps} each")
+    times = {False: [], True: []}
+    b.cs_trace_reset()
+    for i in range(2 * (steps + 1)):
+        fused = i % 2 == 1
+        inp.K.copy_(inp.K0)
+        inp.V.copy_(inp.V0)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        busy_gpu(torch)
+        if fused and i >= 2:
+            b.cs_trace_enable(True)
+        e0.record(stream)
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws_f if fused else ws_p, False, fused, False)
+        e1.record(stream)
+        b.cs_trace_enable(False)
+        torch.cuda.synchronize()
+        if i >= 2:  # the first pair warms up
+            times[fused].append(e0.elapsed_time(e1))
+    trace = b.cs_trace_collect()
+    fm, pm = float(np.median(times[True])), float(np.median(times[False]))
+    log(f"[bench] rho={rho}: fused RoPE compose median {fm:.3f} ms, plain {pm:.3f} ms (alternating steps)")
+    return {"ms": fm, "plain_ms": pm, "trace": trace}
 
 
 def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, paged=False):
@@ -625,9 +666,12 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=No
         line["per_layer_compose_ms" if args.batched_layers else "batched_compose_ms"] = round(other["ms"], 4)
     if fused is not None:
         line["fused_rope_compose_ms"] = round(fused["ms"], 4)
-        fr = fused["trace"].get("rope_scatter_bf16_d128")
-        if fr:
-            line["fused_rope_scatter_us_per_layer"] = round(fr[1] / fr[0] * 1e3, 2)
+        line["fused_rope_plain_alternating_ms"] = round(fused["plain_ms"], 4)
+        for key, name in (("fused_rope_scatter_us_per_layer", "plan_rope_scatter"),
+                          ("fused_rope_sel_attn_us", "sel_attn_mfma")):
+            fr = fused["trace"].get(name)
+            if fr:
+                line[key] = round(fr[1] / fr[0] * 1e3, 2)
     if paged is not None:
         line["paged_compose_ms"] = round(paged["ms"], 4)
         pt = paged["trace"]
