@@ -50,9 +50,9 @@ def parse():
     p.add_argument("--cpu-baseline", type=int, default=1, help="time the CPU oracle on a sample (0: skip)")
     p.add_argument("--batched-layers", type=int, default=0,
                    help="one selective_attend_scatter call over all layers instead of one per layer")
-    p.add_argument("--fused-rope-steps", type=int, default=3,
-                   help="steps also timed through selective_attend_scatter_rope (pre-rotary fresh rows, "
-                        "rotated at the global coordinates; 0: skip)")
+    p.add_argument("--fused-rope-steps", type=int, default=6,
+                   help="steps of each, alternating: selective_attend_scatter_rope (pre-rotary fresh rows, "
+                        "rotated at the global coordinates) and the plain call (0: skip)")
     p.add_argument("--gemm-context", type=int, default=1,
                    help="also time the vendor library's bf16 GEMM on this GPU, as context for the MFMA figure (0: skip)")
     p.add_argument("--paged-steps", type=int, default=3,
