@@ -261,25 +261,29 @@ def bench_fused_vs_plain(inp, w, rho, steps, binding, torch):
     stream = torch.cuda.current_stream()
     log(f"[bench] rho={rho}: n_sel={k}, fused RoPE and plain in alternating steps, steps {steps} each")
     times = {False: [], True: []}
-    b.cs_trace_reset()
+    trace = {}  # the fused steps' kernels (both kinds are traced alike: the trace's events cost time)
     for i in range(2 * (steps + 1)):
         fused = i % 2 == 1
         inp.K.copy_(inp.K0)
         inp.V.copy_(inp.V0)
         torch.cuda.synchronize()
+        b.cs_trace_reset()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         busy_gpu(torch)
-        if fused and i >= 2:
-            b.cs_trace_enable(True)
+        b.cs_trace_enable(True)
         e0.record(stream)
         run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws_f if fused else ws_p, False, fused, False)
         e1.record(stream)
         b.cs_trace_enable(False)
         torch.cuda.synchronize()
+        step_trace = b.cs_trace_collect()
         if i >= 2:  # the first pair warms up
             times[fused].append(e0.elapsed_time(e1))
-    trace = b.cs_trace_collect()
+            if fused:
+                for name, (n_l, ms) in step_trace.items():
+                    n0, ms0 = trace.get(name, (0, 0.0))
+                    trace[name] = (n0 + n_l, ms0 + ms)
     fm, pm = float(np.median(times[True])), float(np.median(times[False]))
     log(f"[bench] rho={rho}: fused RoPE compose median {fm:.3f} ms, plain {pm:.3f} ms (alternating steps)")
     return {"ms": fm, "plain_ms": pm, "trace": trace}

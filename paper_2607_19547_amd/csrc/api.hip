@@ -79,14 +79,11 @@ TraceScope::TraceScope(const char* n, hipStream_t s) : name(n), stream(s), a(nul
   if (!b) {
     if (a) g_pool.push_back(a);
     a = nullptr;
-    return;
   }
-  hipEventRecord(a, s);
 }
 
 TraceScope::~TraceScope() {
   if (!a) return;
-  hipEventRecord(b, stream);
   std::lock_guard<std::mutex> lk(g_trace_mu);
   g_pending.push_back({name, a, b});
 }

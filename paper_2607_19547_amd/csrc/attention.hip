@@ -108,9 +108,9 @@ static void launch_scatter_rows(const ScatterArgs& a, const Rows& rows, hipStrea
   const unsigned blocks = (unsigned)std::min<int64_t>((scatter_items(a) + 255) / 256, 65535);
   TraceScope tr("scatter_rows", s);
   if (scatter_word(a) == 16)
-    hipLaunchKernelGGL((scatter_rows<16, Rows>), dim3(blocks), dim3(256), 0, s, rows, a);
+    CS_LAUNCH(tr, (scatter_rows<16, Rows>), dim3(blocks), dim3(256), 0, s, rows, a);
   else
-    hipLaunchKernelGGL((scatter_rows<4, Rows>), dim3(blocks), dim3(256), 0, s, rows, a);
+    CS_LAUNCH(tr, (scatter_rows<4, Rows>), dim3(blocks), dim3(256), 0, s, rows, a);
 }
 
 
@@ -1310,25 +1310,25 @@ static void launch_mfma_g(const AttnArgs& a, const Rows& rows, const ScatterArgs
   if (ra) {
     TraceScope tr("plan_rope_scatter", s);
     const unsigned blocks = (unsigned)(1 + (int64_t)ra->nblk * a.layers);
-    hipLaunchKernelGGL(plan_rope_scatter<Rows>, dim3(blocks), dim3(1024), 0, s, pa, rows, *ra);
+    CS_LAUNCH(tr, plan_rope_scatter<Rows>, dim3(blocks), dim3(1024), 0, s, pa, rows, *ra);
   } else if (sa) {
     TraceScope tr("plan_scatter", s);
     const unsigned blocks = (unsigned)plan_scatter_blocks(*sa);
     if (scatter_word(*sa) == 16)
-      hipLaunchKernelGGL((plan_scatter<16, Rows>), dim3(blocks), dim3(1024), 0, s, pa, rows, *sa);
+      CS_LAUNCH(tr, (plan_scatter<16, Rows>), dim3(blocks), dim3(1024), 0, s, pa, rows, *sa);
     else
-      hipLaunchKernelGGL((plan_scatter<4, Rows>), dim3(blocks), dim3(1024), 0, s, pa, rows, *sa);
+      CS_LAUNCH(tr, (plan_scatter<4, Rows>), dim3(blocks), dim3(1024), 0, s, pa, rows, *sa);
   } else {
     TraceScope tr("plan_items", s);
-    hipLaunchKernelGGL(plan_items, dim3(1), dim3(1024), 0, s, pa);
+    CS_LAUNCH(tr, plan_items, dim3(1), dim3(1024), 0, s, pa);
   }
   {
     TraceScope tr("sel_attn_mfma", s);
-    hipLaunchKernelGGL((sel_attn_mfma<G, Rows>), dim3((unsigned)mfma_grid(a)), dim3(kThreads), 0, s, a, rows);
+    CS_LAUNCH(tr, (sel_attn_mfma<G, Rows>), dim3((unsigned)mfma_grid(a)), dim3(kThreads), 0, s, a, rows);
   }
   if (a.part_cap > 0) {
     TraceScope tr("sel_attn_combine", s);
-    hipLaunchKernelGGL(sel_attn_combine<G>, dim3((unsigned)combine_grid(a), a.layers), dim3(256), 0, s, a);
+    CS_LAUNCH(tr, sel_attn_combine<G>, dim3((unsigned)combine_grid(a), a.layers), dim3(256), 0, s, a);
   }
 }
 
@@ -1353,10 +1353,10 @@ static void launch_generic(const Geo& g, const GenAttnArgs& a, const Rows& rows,
   static_assert(sizeof(GenAttnArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
   TraceScope tr("sel_attn_generic", s);
   if (g.dtype == CS_BF16)
-    hipLaunchKernelGGL((sel_attn_generic<uint16_t, Rows>), dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a,
+    CS_LAUNCH(tr, (sel_attn_generic<uint16_t, Rows>), dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a,
                        rows);
   else
-    hipLaunchKernelGGL((sel_attn_generic<float, Rows>), dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a,
+    CS_LAUNCH(tr, (sel_attn_generic<float, Rows>), dim3((unsigned)n_sel, g.Hq, layers), dim3(64), 0, s, a,
                        rows);
 }
 

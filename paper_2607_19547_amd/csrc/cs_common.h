@@ -1,6 +1,7 @@
 // Internal helpers shared by the HIP sources of the composition library.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -20,8 +21,10 @@ cs_status check_launch(const char* what);
 cs_status check_grid(int64_t gx, int64_t gy, int64_t gz, int threads, const char* what);
 
 // ------------------------------------------------------------------ tracing
-// While tracing is on, brackets the launches of its scope with two events on
-// `s`; the pair is handed to the collector once both are recorded.
+// While tracing is on, holds two events for the one launch of its scope
+// (CS_LAUNCH): the dispatch itself stamps them at the kernel's start and end,
+// so tracing adds no packets to the stream; the pair goes to the collector
+// when the scope ends.
 struct TraceScope {
   TraceScope(const char* name, hipStream_t s);
   ~TraceScope();
@@ -29,6 +32,11 @@ struct TraceScope {
   hipStream_t stream;
   hipEvent_t a, b;  // both null while tracing is off
 };
+#define CS_LAUNCH(tr, kernel, grid, block, shmem, stream, ...)                                           \
+  do {                                                                                                   \
+    if ((tr).a) hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, (tr).a, (tr).b, 0, __VA_ARGS__); \
+    else hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                             \
+  } while (0)
 
 // ------------------------------------------------------------------ geometry
 struct Geo {

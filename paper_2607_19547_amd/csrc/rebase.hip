@@ -317,7 +317,7 @@ template <typename Rows>
 static void launch_tok_fast(const RebaseTokArgs<64>& a, const Rows& rows, hipStream_t s) {
   static_assert(sizeof(RebaseTokArgs<64>) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
   TraceScope tr("rebase_tokens_bf16_d128", s);
-  hipLaunchKernelGGL(rebase_tokens_bf16_d128<Rows>, dim3((unsigned)((a.T + kTokTB - 1) / kTokTB),
+  CS_LAUNCH(tr, rebase_tokens_bf16_d128<Rows>, dim3((unsigned)((a.T + kTokTB - 1) / kTokTB),
                                                          (unsigned)((a.planes + kTokPG - 1) / kTokPG)),
                      dim3(256), 0, s, a, rows);
 }
@@ -327,9 +327,9 @@ static void launch_tok_generic(const Geo& g, const RebaseTokArgs<256>& a, const 
   static_assert(sizeof(RebaseTokArgs<256>) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
   TraceScope tr("rebase_tokens_generic", s);
   if (g.dtype == CS_BF16)
-    hipLaunchKernelGGL((rebase_tokens_generic<uint16_t, Rows>), dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a, rows);
+    CS_LAUNCH(tr, (rebase_tokens_generic<uint16_t, Rows>), dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a, rows);
   else
-    hipLaunchKernelGGL((rebase_tokens_generic<float, Rows>), dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a, rows);
+    CS_LAUNCH(tr, (rebase_tokens_generic<float, Rows>), dim3((unsigned)g.T, a.planes), dim3(64), 0, s, a, rows);
 }
 
 cs_status launch_rebase_tokens(const Geo& g, const CacheView& cv, const int32_t* off, const double* theta,
@@ -399,7 +399,7 @@ cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, c
         for (int x = 0; x < 3; ++x) a.off[q][x] = off[3 * c + x];
       }
       TraceScope tr("rebase_bf16_d128", s);
-      hipLaunchKernelGGL(rebase_bf16_d128, dim3((unsigned)(tb_fast * pg_fast * nc)), dim3(256), 0, s, a);
+      CS_LAUNCH(tr, rebase_bf16_d128, dim3((unsigned)(tb_fast * pg_fast * nc)), dim3(256), 0, s, a);
     } else {
       RebaseGenArgs a;
       a.T = g.T;
@@ -419,9 +419,9 @@ cs_status launch_rebase(const Geo& g, const CacheView& cv, const int32_t* off, c
       }
       TraceScope tr("rebase_generic", s);
       if (g.dtype == CS_BF16)
-        hipLaunchKernelGGL(rebase_generic<uint16_t>, dim3(a.tblocks * planes, nc), dim3(256), 0, s, a);
+        CS_LAUNCH(tr, rebase_generic<uint16_t>, dim3(a.tblocks * planes, nc), dim3(256), 0, s, a);
       else
-        hipLaunchKernelGGL(rebase_generic<float>, dim3(a.tblocks * planes, nc), dim3(256), 0, s, a);
+        CS_LAUNCH(tr, rebase_generic<float>, dim3(a.tblocks * planes, nc), dim3(256), 0, s, a);
     }
     st = check_launch("rebase kernel launch");
     if (st) return st;

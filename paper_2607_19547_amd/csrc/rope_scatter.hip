@@ -85,9 +85,9 @@ static void launch_rs_generic(const Geo& g, const RopeScatterGenArgs& a, const R
   static_assert(sizeof(RopeScatterGenArgs) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
   TraceScope tr("rope_scatter_generic", s);
   if (g.dtype == CS_BF16)
-    hipLaunchKernelGGL((rope_scatter_generic<uint16_t, Rows>), dim3((unsigned)n_sel, layers), dim3(64), 0, s, a, rows);
+    CS_LAUNCH(tr, (rope_scatter_generic<uint16_t, Rows>), dim3((unsigned)n_sel, layers), dim3(64), 0, s, a, rows);
   else
-    hipLaunchKernelGGL((rope_scatter_generic<float, Rows>), dim3((unsigned)n_sel, layers), dim3(64), 0, s, a, rows);
+    CS_LAUNCH(tr, (rope_scatter_generic<float, Rows>), dim3((unsigned)n_sel, layers), dim3(64), 0, s, a, rows);
 }
 
 cs_status launch_rope_scatter(const Geo& g, const CacheView& cv, int lb, int le, const int32_t* sel, int64_t n_sel,

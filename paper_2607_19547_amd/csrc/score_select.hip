@@ -271,15 +271,15 @@ static void launch_score(const Geo& g, const Rows& rows, int score_layer, const 
   TraceScope tr("deviation_score", s);
   if (g.dtype == CS_BF16 && g.D == 128) {
     const int64_t blocks = (g.n + 15) / 16;
-    hipLaunchKernelGGL(deviation_score_bf16_d128<Rows>, dim3((unsigned)blocks), dim3(256), 0, s, rows,
+    CS_LAUNCH(tr, deviation_score_bf16_d128<Rows>, dim3((unsigned)blocks), dim3(256), 0, s, rows,
                        (const uint16_t*)k_fresh, scores, score_layer, g.n, g.cs1, g.Hkv);
   } else {
     const int64_t blocks = (g.n + 3) / 4;
     if (g.dtype == CS_BF16)
-      hipLaunchKernelGGL((deviation_score<uint16_t, Rows>), dim3((unsigned)blocks), dim3(256), 0, s, rows,
+      CS_LAUNCH(tr, (deviation_score<uint16_t, Rows>), dim3((unsigned)blocks), dim3(256), 0, s, rows,
                          (const uint16_t*)k_fresh, scores, score_layer, g.n, g.cs1, g.Hkv, g.D);
     else
-      hipLaunchKernelGGL((deviation_score<float, Rows>), dim3((unsigned)blocks), dim3(256), 0, s, rows,
+      CS_LAUNCH(tr, (deviation_score<float, Rows>), dim3((unsigned)blocks), dim3(256), 0, s, rows,
                          (const float*)k_fresh, scores, score_layer, g.n, g.cs1, g.Hkv, g.D);
   }
 }
@@ -296,10 +296,10 @@ cs_status launch_score_select(const Geo& g, const CacheView& cv, int score_layer
   {
     TraceScope tr("radix_select_topk", s);
     if (g.n <= (int64_t)kSelHeld * kSelThreads)
-      hipLaunchKernelGGL(radix_select_topk<true>, dim3(1), dim3(kSelThreads), 0, s, scores, (int)g.n, (int)k_sel,
+      CS_LAUNCH(tr, radix_select_topk<true>, dim3(1), dim3(kSelThreads), 0, s, scores, (int)g.n, (int)k_sel,
                          (int)g.cs1, sel);
     else
-      hipLaunchKernelGGL(radix_select_topk<false>, dim3(1), dim3(kSelThreads), 0, s, scores, (int)g.n,
+      CS_LAUNCH(tr, radix_select_topk<false>, dim3(1), dim3(kSelThreads), 0, s, scores, (int)g.n,
                          (int)k_sel, (int)g.cs1, sel);
   }
   return check_launch("top-k select launch");
