@@ -344,13 +344,16 @@ const char* cs_last_error(void);
 
 /* ---------------------------------------------------------------------------
  * Kernel tracing (measurement aid, off by default).
- * While enabled, every kernel the library launches is bracketed by a pair of
- * hipEvents on its own stream.  cs_trace_collect() synchronises those events
- * and accumulates, per kernel name, the number of launches and their total
+ * While enabled, every kernel the library launches carries a pair of
+ * hipEvents that its own dispatch stamps at the kernel's start and end
+ * (hipExtLaunchKernel: no extra packets on the stream, so tracing leaves the
+ * timeline as it is).  cs_trace_collect() synchronises those events and
+ * accumulates, per kernel name, the number of launches and their total
  * duration.  The trace state is shared by all threads and guarded by a
- * lock; a kernel's events reach the collector once both are recorded, so a
- * collect running beside launches on other threads never waits on a half-
- * recorded pair.  A collect that fails keeps the launches it had not reached. */
+ * lock; a kernel's events reach the collector once its launch is enqueued,
+ * so a collect running beside launches on other threads never waits on a
+ * half-enqueued pair.  A collect that fails keeps the launches it had not
+ * reached. */
 cs_status cs_trace_enable(int32_t on);
 cs_status cs_trace_collect(void);
 int32_t cs_trace_count(void);
