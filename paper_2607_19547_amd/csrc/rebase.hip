@@ -169,8 +169,18 @@ __global__ __launch_bounds__(256) void rebase_generic(const RebaseGenArgs a) {
 // the block's cos/sin table in LDS (angles in float64, the same reduction as
 // above), then streams the block's rows of its planes.  Rows whose token has
 // offset (0, 0, 0) are not touched.
-constexpr int kTokTB = 64;  // tokens per workgroup
-constexpr int kTokPG = 8;   // planes per workgroup
+// Workgroup shape (tokens x planes) per cache layout, measured on the 65k
+// cache under scalar re-basing: contiguous 32 x 4 (64 x 8: 440 us, 16 x 8:
+// 595 us, 32 x 4: 416 us), chunk buffers 16 x 8 (64 x 8: 452 us, 32 x 4:
+// 534 us, 16 x 8: 412 us).
+template <typename Rows>
+struct TokShape {
+  static constexpr int TB = 32, PG = 4;
+};
+template <int N>
+struct TokShape<PagedRowsT<N>> {
+  static constexpr int TB = 16, PG = 8;
+};
 constexpr int kTokTabW = 65;  // table row stride (float2): one pad entry spreads the LDS banks
 
 template <int P_MAX>
@@ -185,7 +195,9 @@ struct RebaseTokArgs {
 template <typename Rows>
 __global__ __launch_bounds__(256) void rebase_tokens_bf16_d128(const RebaseTokArgs<64> a, const Rows rows) {
   constexpr bool kPaged = !std::is_same<Rows, FlatRows>::value;
+  constexpr int kTokTB = TokShape<Rows>::TB, kTokPG = TokShape<Rows>::PG;
   constexpr int kU = (kTokPG * kTokTB) / 32;  // rows per lane group
+  static_assert(kPaged || kU % 4 == 0, "the contiguous path turns whole batches of four rows per lane group");
   __shared__ float2 tab[kTokTB * kTokTabW];
   __shared__ int moved[kTokTB];
   __shared__ char* row0[kTokTB];         // the token's row in plane 0
@@ -317,9 +329,9 @@ template <typename Rows>
 static void launch_tok_fast(const RebaseTokArgs<64>& a, const Rows& rows, hipStream_t s) {
   static_assert(sizeof(RebaseTokArgs<64>) + sizeof(Rows) <= 4096, "kernel arguments within 4 KB");
   TraceScope tr("rebase_tokens_bf16_d128", s);
-  CS_LAUNCH(tr, rebase_tokens_bf16_d128<Rows>, dim3((unsigned)((a.T + kTokTB - 1) / kTokTB),
-                                                         (unsigned)((a.planes + kTokPG - 1) / kTokPG)),
-                     dim3(256), 0, s, a, rows);
+  constexpr int TB = TokShape<Rows>::TB, PG = TokShape<Rows>::PG;
+  CS_LAUNCH(tr, rebase_tokens_bf16_d128<Rows>, dim3((unsigned)((a.T + TB - 1) / TB), (unsigned)((a.planes + PG - 1) / PG)),
+            dim3(256), 0, s, a, rows);
 }
 
 template <typename Rows>
@@ -336,7 +348,9 @@ cs_status launch_rebase_tokens(const Geo& g, const CacheView& cv, const int32_t*
                                hipStream_t s, bool check_only) {
   const int64_t planes = (int64_t)g.L * g.Hkv;
   const bool fast = g.dtype == CS_BF16 && g.D == 128;
-  cs_status st = fast ? check_grid((g.T + kTokTB - 1) / kTokTB, (planes + kTokPG - 1) / kTokPG, 1, 256, "per-token rebase")
+  const int TB = cv.paged ? TokShape<PagedRowsT<kMaxPages>>::TB : TokShape<FlatRows>::TB;
+  const int PG = cv.paged ? TokShape<PagedRowsT<kMaxPages>>::PG : TokShape<FlatRows>::PG;
+  cs_status st = fast ? check_grid((g.T + TB - 1) / TB, (planes + PG - 1) / PG, 1, 256, "per-token rebase")
                       : check_grid(g.T, planes, 1, 64, "per-token rebase");
   if (st || check_only) return st;
   if (fast) {
