@@ -202,7 +202,8 @@ def main():
     w = synth.WORKLOADS[args.workload]
     rho = w.rho if args.rho is None else args.rho
     inp = Inputs(w, torch, binding, synth)
-    result = bench_rho(inp, w, rho, args.steps, args.warmup, binding, torch, bool(args.batched_layers))
+    result = bench_rho(inp, w, rho, args.steps, args.warmup, binding, torch, bool(args.batched_layers),
+                       untraced_steps=args.steps)
     rho1 = None
     if args.rho1_steps > 0 and rho != 1.0:
         rho1 = bench_rho(inp, w, 1.0, args.rho1_steps, 1, binding, torch, bool(args.batched_layers))
@@ -289,7 +290,7 @@ def bench_fused_vs_plain(inp, w, rho, steps, binding, torch):
     return {"ms": fm, "plain_ms": pm, "trace": trace}
 
 
-def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, paged=False):
+def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, paged=False, untraced_steps=0):
     b = binding
     n = w.n_candidates
     scores = torch.empty(n, dtype=torch.float32, device="cuda")
@@ -342,6 +343,20 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, 
         times.append(e0.elapsed_time(e1))
     wall = time.perf_counter() - wall0
     trace = b.cs_trace_collect()
+    # The same steps without the per-kernel trace, whose events cost the host ~14 us per launch: where
+    # a layer call's GPU work is short (the 8k-token cache), the traced steps wait on the host.
+    untraced = []
+    for _ in range(untraced_steps):
+        restore()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        busy_gpu(torch)
+        e0.record(stream)
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused, paged)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        untraced.append(e0.elapsed_time(e1))
     # algorithmic work of the step (from the selection of the last step; outside the timed region)
     g = sel[:k].cpu().numpy().astype(np.int64)
     visible = int(np.sum(g + 1))
@@ -352,8 +367,10 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, 
     rebase_bytes = 2 * w.n_layers * w.n_kv_heads * rot_tokens * w.head_dim * 2   # read + write, bf16
     res = dict(rho=rho, n_sel=k, ms=float(np.median(times)), ms_mean=float(np.mean(times)),
                ms_min=float(np.min(times)), wall_s=wall, steps=steps, trace=trace,
-               attn_flops_per_layer=attn_flops_per_layer, rebase_bytes=rebase_bytes, visible=visible)
-    log(f"[bench] rho={rho}: compose median {res['ms']:.3f} ms (min {res['ms_min']:.3f}); kernels:")
+               attn_flops_per_layer=attn_flops_per_layer, rebase_bytes=rebase_bytes, visible=visible,
+               ms_untraced=float(np.median(untraced)) if untraced else None)
+    log(f"[bench] rho={rho}: compose median {res['ms']:.3f} ms (min {res['ms_min']:.3f})"
+        + (f", untraced {res['ms_untraced']:.3f} ms" if untraced else "") + "; kernels:")
     for name, (cnt, tot) in sorted(trace.items(), key=lambda kv: -kv[1][1]):
         log(f"    {name:24s} launches {cnt:5d}  avg {tot / cnt * 1e3:9.1f} us  total/step {tot / steps:8.3f} ms")
     return res
@@ -666,6 +683,8 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=No
             "avg_launch_us": round(reb_avg_s * 1e6, 2),
         },
     }
+    if r.get("ms_untraced") is not None:
+        line["compose_untraced_ms"] = round(r["ms_untraced"], 4)
     if other is not None:
         line["per_layer_compose_ms" if args.batched_layers else "batched_compose_ms"] = round(other["ms"], 4)
     if fused is not None:

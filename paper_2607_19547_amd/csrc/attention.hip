@@ -622,8 +622,10 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
 
   // The workgroup stays resident and takes items one after another from its
   // XCD's queue (then from the others'), through one atomic counter per
-  // queue.  The next item is claimed while an item's results are written, and
-  // its first two key tiles are fetched before its queries are loaded.
+  // queue.  The next item is claimed during an item's last key tiles and
+  // started (its descriptor and first two key tiles) before the item's
+  // results are written; its first two key tiles are fetched before its
+  // queries are loaded.
   //
   // Registers are the limit of this kernel (two wavefronts per SIMD), so
   // nothing that only the per-item code needs is kept in registers across the
@@ -672,6 +674,14 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     jq = __builtin_amdgcn_readfirstlane(s_claim[1]);
     __syncthreads();  // s_claim is reused by the next claim
     return it;
+  };
+  // Thread 0's claim of the next queue position, read later: the lane offset
+  // the compiler cannot see is zero keeps it from turning the add into a
+  // wavefront-wide atomic whose result it reads (and waits for) at once.
+  auto claim_add = [&](int* ctr) -> int {
+    int z;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+    return atomicAdd(ctr + z, 1);
   };
   auto claim_one = [&](const AttnArgs& A) -> int {
     int got = 0;
@@ -739,10 +749,9 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     fetch(key_begin + kKT, up_k1, lo_v1);
     return true;
   };
-  auto next_item = [&](const AttnArgs& A, int got) {  // claims until an item starts; false when none is left
+  auto begin_next = [&](const AttnArgs& A, int got) {  // claims until an item starts; false when none is left
     int item = claim_rest(A, got);
     while (item >= 0 && !start_item(A, item)) item = claim_one(A);
-    __syncthreads();  // s_it is written
     return item >= 0;
   };
 
@@ -764,7 +773,9 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
   const float sc = a.scale_log2;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  if (!next_item(a, tid == 0 ? atomicAdd(&plan_view(a.plan, a.n_tiles).hdr[jq], 1) : 0)) return;  // every queue is empty
+  if (!begin_next(a, tid == 0 ? atomicAdd(&plan_view(a.plan, a.n_tiles).hdr[jq], 1) : 0)) return;  // every queue is empty
+  __syncthreads();  // s_it is written
+  int got = 0;      // thread 0: the next claim, made during the item's last key tiles
 
   while (true) {
     int g_q = -1, g_wmin, g_wmax, key_begin, n_kt;
@@ -772,17 +783,19 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     {
       const AttnArgs A = args();
       key_begin = it_field(4);
-      fetch(key_begin + 2 * kKT, up_k2, lo_v2);
       const int lrel = it_field(0), oi = it_field(1), kv = it_field(2);
       const int key_end = it_field(5);
       n_kt = key_end > key_begin ? (key_end - key_begin + kKT - 1) / kKT : 0;
       const int ln = lane_id(), lq = ln & 31;
       const int64_t m = (A.n_tiles - 1 - oi) * RT + wave * RW + lq / G;
       const int h = kv * G + lq % G;
-      if (m < A.n_sel) {
-        const int t = A.sel[m];
-        if (t >= A.cs1 && t < A.T) g_q = t;
-      }
+      // the selected token is loaded before key tile 2's DMA is issued, so
+      // that the wait for it (and the query load behind it) does not also
+      // wait for that DMA
+      const int t = A.sel[min<int64_t>(m, A.n_sel - 1)];
+      asm volatile("" ::: "memory");
+      fetch(key_begin + 2 * kKT, up_k2, lo_v2);
+      if (m < A.n_sel && t >= A.cs1 && t < A.T) g_q = t;
       // the wavefront's smallest and largest token: masking starts at the
       // tile that reaches past the smallest, arithmetic stops after the largest
       g_wmin = g_q >= 0 ? g_q : 0x7fffffff;
@@ -966,10 +979,16 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     };
 
     f32x16 sa0, sa1, sb0, sb1;
+    // The next item is claimed at the start of the last group of four steps
+    // that leaves at least two steps, so that the claim's round trip overlaps
+    // them (an earlier claim would hold the item back from idle workgroups
+    // for longer).
+    const int claim_at = max(0, (n_kt - 2) & ~3);
     asm volatile("s_waitcnt vmcnt(4)" ::: "memory");  // tiles 0 and 1 and the queries have landed
     __builtin_amdgcn_s_barrier();
     qk(I0{}, sa0, sa1);
     for (int i = 0; i < n_kt; i += 4) {
+      if (i == claim_at && tid == 0) got = claim_add(plan_view(args().plan, 0).hdr + jq);
       step(I0{}, I1{}, I3{}, i, sa0, sa1, sb0, sb1);
       if (i + 1 >= n_kt) break;
       step(I1{}, I2{}, I0{}, i + 1, sb0, sb1, sa0, sa1);
@@ -981,16 +1000,18 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this item's DMA is complete
     __builtin_amdgcn_s_barrier();                     // and every wavefront is done with the ring
 
-    // Epilogue.  The next item is claimed first; its answer is read after
-    // this item's results are on their way.
+    // Epilogue.  The next item (claimed in the tile loop, or here if the item
+    // had no key tiles) is started first: its descriptor, buffer ranges and
+    // key tiles 0 and 1 into ring slots 0 and 1, while this item's results
+    // pass through slots 2 and 3.
     const AttnArgs A = args();
     const PlanView pv = plan_view(A.plan, A.n_tiles);
-    int got = 0;
-    if (tid == 0) got = atomicAdd(&pv.hdr[jq], 1);
-    const int lrel = it_field(0), oi = it_field(1), kv = it_field(2);
+    if (n_kt == 0 && tid == 0) got = claim_add(&pv.hdr[jq]);
+    const int lrel = it_field(0), oi = it_field(1), kv = it_field(2), piece_f = it_field(3);
+    const bool more = begin_next(A, got);
     const int layer = A.lb + lrel;
     const int nsp = pv.nsp[oi];
-    const int piece = min(it_field(3), nsp - 1);  // (a bound, as in start_item)
+    const int piece = min(piece_f, nsp - 1);  // (a bound, as in start_item)
     const int64_t m0 = (A.n_tiles - 1 - oi) * RT;
     const bool valid = g_q >= 0;
     const int el = lane_id(), eq = el & 31, ehi = el >> 5;
@@ -1066,10 +1087,10 @@ __global__ __launch_bounds__(kThreads) void sel_attn_mfma(const AttnArgs a, cons
         *(u32x4*)(pp + R * 128 + 8 * c) = get(R, c);
       }
     }
-    // every wavefront is done with ring slots 2 and 3 and with s_it before
-    // the next item is written there
+    // every wavefront is done with ring slots 2 and 3 before the next item's
+    // key tile 2 is fetched there, and s_it holds the next item
     __syncthreads();
-    if (!next_item(A, got)) break;
+    if (!more) break;
   }
 }
 
