@@ -199,7 +199,8 @@ cs_status score_deviation_topk(const cs_geometry* g, const void* k_cache,
  *                  layer_begin: the attention's partials plus, for bf16 with
  *                  head_dim 128, the cos/sin table (n_sel x D/2 x 8 bytes),
  *                  otherwise the rotated queries (n_layers x H_q x n_sel x D
- *                  elements)
+ *                  elements); the work plan is kept from call to call as in
+ *                  selective_attend_scatter's workspace
  *   other arguments as for selective_attend_scatter.
  * Errors: CS_ERR_INVALID_ARGUMENT, CS_ERR_WORKSPACE_TOO_SMALL, CS_ERR_HIP. */
 cs_status selective_attend_scatter_rope_workspace(const cs_geometry* g, int64_t n_sel,
@@ -249,7 +250,15 @@ cs_status selective_attend_scatter_rope(const cs_geometry* g, void* k_cache,
  *   workspace      DEVICE scratch, >= selective_attend_scatter_workspace()
  *                  for the same n_sel and n_layers_per_call >= layer_end -
  *                  layer_begin (the size grows with the layer count); no
- *                  initial contents needed, not kept between calls
+ *                  initial contents needed.  The call leaves its work plan at
+ *                  the start of the workspace; a later call that finds there
+ *                  a plan made from the same inputs (the row tiles' last
+ *                  selected tokens, the row-tile and KV-head counts, the
+ *                  partial-slot budget), whose checksum holds, keeps it
+ *                  instead of planning again, so the layer calls of one
+ *                  composition plan once.  Any other contents are
+ *                  overwritten: the caller may use the workspace for anything
+ *                  between calls.
  * Errors: CS_ERR_INVALID_ARGUMENT, CS_ERR_WORKSPACE_TOO_SMALL, CS_ERR_HIP. */
 cs_status selective_attend_scatter_workspace(const cs_geometry* g, int64_t n_sel,
                                              int32_t n_layers_per_call,
@@ -274,7 +283,8 @@ cs_status selective_attend_scatter(const cs_geometry* g, void* k_cache,
  * device address is looked up once per GPU, on the first call with that GPU
  * current.  Every call on a GPU shares that GPU's array: calls that overlap
  * on one GPU (two streams, two threads) race and give wrong results.  Nothing
- * needs clearing between calls.
+ * needs clearing between calls; the plan left in the array is kept by a later
+ * call with the same inputs, as in a workspace.
  *
  * When the call's plan and partials would exceed the array, the key pieces
  * of long row tiles are made longer (fewer partials), so the output then

@@ -212,7 +212,8 @@ __device__ __forceinline__ void stage_dma(__amdgpu_buffer_rsrc_t rk, __amdgpu_bu
 // first; the last quarter is then reordered longest first, so a launch ends
 // on its shortest items.  The pieces of a cut row tile leave partial (O, max,
 // sum) in fixed workspace slots that sel_attn_combine merges in piece order.
-constexpr int kPlanHdr = 16;    // header ints, see PlanView
+constexpr int kPlanHdr = 32;    // header ints, see PlanView
+constexpr int kPlanMagic = 0x43530231;  // marks a header the planning kernel wrote
 constexpr int kPlanCUs = 256;   // CU count S is derived from (a constant: results do not depend on the device)
 constexpr int kItemsPerCU = 6;  // target items per CU when row tiles must be cut
 // Smallest piece: 16 key tiles.  Short caches and small rho leave few items
@@ -230,7 +231,10 @@ constexpr int kXcds = 8;
 struct PlanView {
   int* hdr;   // [0, 8) queue counters, [8] nq, [9] S, [10] cut row tiles, [11] most pieces,
               // [12] items per queue and layer,
-              // [14] offset of the item descriptors (ints from the plan's start)
+              // [14] offset of the item descriptors (ints from the plan's start);
+              // [16, 24): what the plan was made from and its checksum (kPlanMagic,
+              // n_tiles, RT, H_kv, part_cap, desc_off, two checksum words), [24] 1 when
+              // the last planning launch reused the plan, 0 when it made it
   int* nu;    // [n_tiles] key tiles of row tile i (longest first)
   int* nsp;   // [n_tiles] pieces of row tile i
   int* ppre;  // [n_tiles + 1] first partial slot of row tile i (prefix sums of H_kv x pieces over cut row tiles)
@@ -297,13 +301,56 @@ __device__ __forceinline__ int block_scan(int x, int* wsum, int* base) {
 struct PlanArgs {
   const int32_t* sel;
   int64_t n_sel, n_tiles, T;
-  int RT, Hkv, layers, part_cap;
+  int RT, Hkv, part_cap;
+  int pj_cap, desc_cap;  // ints of the piece sections and item descriptors the workspace holds
   int desc_off;  // where the item descriptors start
   int* plan;
 };
-__device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_t n_tiles, int RT, int64_t T, int Hkv,
-                          int layers, int part_cap, int desc_off, int* __restrict__ plan) {
+// Two checksum words over the plan's ints that the attention and combine
+// kernels read (header [8, 16), pieces and partial slots per row tile, piece
+// sections, item descriptors), each int weighted by its position: unsigned
+// sums, so the order of the terms does not matter.
+__device__ __forceinline__ uint2 plan_checksum(const int* plan, int64_t n_tiles, int nj, int desc_off, int per_q,
+                                               unsigned* red) {
+  unsigned c1 = 0, c2 = 0;
+  auto add = [&](int64_t b, int64_t e) {
+    for (int64_t i = b + threadIdx.x; i < e; i += 1024) {
+      const unsigned v = (unsigned)plan[i], x = (unsigned)i;
+      c1 += v * (2u * x + 1u);
+      c2 += (v ^ (x * 0x9E3779B9u)) * 0x85EBCA6Bu + x;
+    }
+  };
+  const PlanView pv = plan_view(const_cast<int*>(plan), n_tiles);
+  add(8, 16);
+  add(pv.nsp - plan, pv.pj - plan);  // nsp and ppre
+  add(pv.pj - plan, pv.pj - plan + nj + 1);
+  add(desc_off, desc_off + 4 * (int64_t)per_q);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    c1 += (unsigned)__shfl_xor((int)c1, o);
+    c2 += (unsigned)__shfl_xor((int)c2, o);
+  }
+  __syncthreads();  // red may still be read by an earlier reduction
+  if ((threadIdx.x & 63) == 0) {
+    red[threadIdx.x >> 6] = c1;
+    red[16 + (threadIdx.x >> 6)] = c2;
+  }
+  __syncthreads();
+  uint2 r = make_uint2(0u, 0u);
+  for (int w = 0; w < 16; ++w) {
+    r.x += red[w];
+    r.y += red[16 + w];
+  }
+  return r;
+}
+
+__device__ void plan_body(const PlanArgs& p) {
+  const int32_t* __restrict__ sel = p.sel;
+  const int64_t n_sel = p.n_sel, n_tiles = p.n_tiles, T = p.T;
+  const int RT = p.RT, Hkv = p.Hkv, part_cap = p.part_cap, desc_off = p.desc_off;
+  int* __restrict__ plan = p.plan;
   __shared__ int red[16];
+  __shared__ unsigned red_u[32];
   __shared__ int wsum[16];
   __shared__ int s_base;
   // the arrays the plan reads back live in LDS when they fit (global memory
@@ -320,7 +367,14 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
   // for any other list it keeps n_i non-increasing along the longest-first
   // order, which the placement of the items below relies on (the cut row
   // tiles lead, and every queue position is written exactly once).
-  int sum = 0;
+  //
+  // The plan is a function of these counts and of n_tiles, RT, H_kv, part_cap
+  // and desc_off alone.  The workspace may still hold the plan of an earlier
+  // call (the layer calls of one composition share their selection): when it
+  // was made from the same counts and sizes and its checksum holds, it is
+  // kept and only its claim counters are cleared.  The counts are kept in the
+  // plan for that comparison.
+  int sum = 0, diff = 0;
   if (tid == 0) s_base = 0;
   __syncthreads();
   for (int64_t b = 0; b < n_tiles; b += 1024) {
@@ -333,12 +387,34 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
     }
     v = block_scan<true>(v, wsum, &s_base);
     if (t < n_tiles) {
-      nu[n_tiles - 1 - t] = v;
+      const int64_t i = n_tiles - 1 - t;
+      diff |= pv.nu[i] != v;  // (the stored count, read before it is replaced)
+      pv.nu[i] = v;
+      if (in_lds) l_nu[i] = v;
       sum += v;
     }
   }
   const int nmax = s_base;  // (block_scan ends on a barrier)
   const int W1 = block_reduce(sum, false, red);
+  {
+    const int* hdr = pv.hdr;  // (every thread reads the same values: the decision is uniform)
+    bool same = block_reduce(diff, true, red) == 0 && hdr[16] == kPlanMagic && hdr[17] == n_tiles &&
+                hdr[18] == RT && hdr[19] == Hkv && hdr[20] == part_cap && hdr[21] == desc_off;
+    if (same) {
+      const int nj_s = hdr[11], per_q_s = hdr[12];
+      same = nj_s >= 0 && nj_s < p.pj_cap && per_q_s >= 0 && 4 * (int64_t)per_q_s <= p.desc_cap;
+      if (same) {
+        const uint2 c = plan_checksum(plan, n_tiles, nj_s, desc_off, per_q_s, red_u);
+        same = c.x == (unsigned)hdr[22] && c.y == (unsigned)hdr[23];
+      }
+    }
+    if (same) {
+      __syncthreads();  // every thread has read the header
+      if (tid < kXcds) pv.hdr[tid] = 0;  // the queues' claim counters
+      if (tid == 0) pv.hdr[24] = 1;
+      return;
+    }
+  }
   // piece size: about kItemsPerCU items per CU, raised until the partial
   // slots fit in part_cap (no cut at all always fits)
   const int64_t per = (int64_t)kPlanCUs * kItemsPerCU;
@@ -456,42 +532,57 @@ __device__ void plan_body(const int32_t* __restrict__ sel, int64_t n_sel, int64_
       put(pos, make_int4(i, kvl, 0, nu[i]));
     }
   }
-  if (!sort_tail) return;  // (uniform)
-  // counting sort of the tail by length (at most S key tiles), longest first,
-  // in 256 buckets
-  __syncthreads();
-  const int nt = per_q_all - r0;
-  int shift = 0;
-  while ((S >> shift) > 255) ++shift;
-  auto bucket = [&](int4 d) { return 255 - min((d.w - d.z) >> shift, 255); };
-  for (int t = tid; t < nt; t += 1024) atomicAdd(&l_bkt[bucket(l_desc[t])], 1);
-  __syncthreads();
-  if (tid < 64) {  // exclusive scan of the 256 bucket counts by one wavefront
-    int c4[4], tot = 0;
+  if (sort_tail) {  // (uniform)
+    // counting sort of the tail by length (at most S key tiles), longest
+    // first, in 256 buckets
+    __syncthreads();
+    const int nt = per_q_all - r0;
+    int shift = 0;
+    while ((S >> shift) > 255) ++shift;
+    auto bucket = [&](int4 d) { return 255 - min((d.w - d.z) >> shift, 255); };
+    for (int t = tid; t < nt; t += 1024) atomicAdd(&l_bkt[bucket(l_desc[t])], 1);
+    __syncthreads();
+    if (tid < 64) {  // exclusive scan of the 256 bucket counts by one wavefront
+      int c4[4], tot = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) tot += c4[q] = l_bkt[4 * tid + q];
-    int incl = tot;
+      for (int q = 0; q < 4; ++q) tot += c4[q] = l_bkt[4 * tid + q];
+      int incl = tot;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(incl, o);
-      if (tid >= o) incl += y;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (tid >= o) incl += y;
+      }
+      int run = incl - tot;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        l_bkt[4 * tid + q] = run;
+        run += c4[q];
+      }
     }
-    int run = incl - tot;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      l_bkt[4 * tid + q] = run;
-      run += c4[q];
+    __syncthreads();
+    for (int t = tid; t < nt; t += 1024) {
+      const int4 d = l_desc[t];
+      desc[r0 + atomicAdd(&l_bkt[bucket(d)], 1)] = d;
     }
   }
-  __syncthreads();
-  for (int t = tid; t < nt; t += 1024) {
-    const int4 d = l_desc[t];
-    desc[r0 + atomicAdd(&l_bkt[bucket(d)], 1)] = d;
+  // what the plan was made from, and its checksum, for the next call to compare
+  __syncthreads();  // every part of the plan is written
+  const uint2 c = plan_checksum(plan, n_tiles, nj, desc_off, per_q_all, red_u);
+  if (tid == 0) {
+    pv.hdr[16] = kPlanMagic;
+    pv.hdr[17] = (int)n_tiles;
+    pv.hdr[18] = RT;
+    pv.hdr[19] = Hkv;
+    pv.hdr[20] = part_cap;
+    pv.hdr[21] = desc_off;
+    pv.hdr[22] = (int)c.x;
+    pv.hdr[23] = (int)c.y;
+    pv.hdr[24] = 0;
   }
 }
 
 __global__ __launch_bounds__(1024) void plan_items(const PlanArgs p) {
-  plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.desc_off, p.plan);
+  plan_body(p);
 }
 
 // The plan (workgroup 0) and the scatter of the call's fresh rows (the other
@@ -500,7 +591,7 @@ __global__ __launch_bounds__(1024) void plan_items(const PlanArgs p) {
 template <int W, typename Rows>
 __global__ __launch_bounds__(1024) void plan_scatter(const PlanArgs p, const Rows rows, const ScatterArgs sa) {
   if (blockIdx.x == 0) {
-    plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.desc_off, p.plan);
+    plan_body(p);
     return;
   }
   scatter_body<W>(rows, sa, (int64_t)(blockIdx.x - 1) * 1024 + threadIdx.x, (int64_t)(gridDim.x - 1) * 1024);
@@ -584,7 +675,7 @@ __device__ void rope_rows_body(const RopeRowsArgs& a, const Rows& rows, int blk,
 template <typename Rows>
 __global__ __launch_bounds__(1024) void plan_rope_scatter(const PlanArgs p, const Rows rows, const RopeRowsArgs ra) {
   if (blockIdx.x == 0) {
-    plan_body(p.sel, p.n_sel, p.n_tiles, p.RT, p.T, p.Hkv, p.layers, p.part_cap, p.desc_off, p.plan);
+    plan_body(p);
     return;
   }
   const int b = blockIdx.x - 1;
@@ -1254,6 +1345,18 @@ __global__ __launch_bounds__(64) void sel_attn_generic(const GenAttnArgs a, cons
 // ============================================================== planning & launch
 static int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
+// A piece has at least kMinPiece key tiles, so a row tile has at most
+// ceil(ceil(T / 64) / kMinPiece) pieces (and at most kMaxPieces).
+static int64_t plan_max_pieces(int64_t T) {
+  return std::min<int64_t>(kMaxPieces, ((T + kKT - 1) / kKT + kMinPiece - 1) / kMinPiece);
+}
+// Items per queue and layer: at most one per row tile and KV head of the
+// queue, plus the extra pieces of cut row tiles (bounded by part_cap).
+static int64_t plan_per_q_bound(int64_t n_tiles, int Hkv, int part_cap) {
+  const int nq = n_queues(Hkv);
+  return (n_tiles * Hkv + part_cap + nq - 1) / nq;
+}
+
 AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call, int64_t max_part_slots) {
   AttnPlan p{};
   // (buffer loads address one [T][128] bf16 plane, plus three tiles of
@@ -1266,10 +1369,9 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call, int64_
   }
   p.rows_per_tile = kWaves * (32 / g.G);
   p.n_tiles = (n_sel + p.rows_per_tile - 1) / p.rows_per_tile;
-  // Partial slots: a piece has at least kMinPiece key tiles, so a row tile
-  // has at most ceil(ceil(T / 64) / kMinPiece) pieces; the plan keeps the
-  // total under kPartCap per layer by enlarging the pieces.
-  const int64_t max_pieces = std::min<int64_t>(kMaxPieces, ((g.T + kKT - 1) / kKT + kMinPiece - 1) / kMinPiece);
+  // Partial slots: the plan keeps the total under kPartCap per layer by
+  // enlarging the pieces.
+  const int64_t max_pieces = plan_max_pieces(g.T);
   // the plan counts key tiles of a layer, and items of a call, in 32-bit integers
   if (p.n_tiles * ((g.T + kKT - 1) / kKT) * g.Hkv >= (int64_t(1) << 31) ||
       p.n_tiles * g.Hkv * std::max<int64_t>(1, max_pieces) * std::max(1, layers_per_call) >= (int64_t(1) << 31)) {
@@ -1283,8 +1385,7 @@ AttnPlan plan_attention(const Geo& g, int64_t n_sel, int layers_per_call, int64_
   // a cut row tile fills at least 2 H_kv slots: fewer slots allow no cut at all
   if (p.part_cap < 2 * g.Hkv) p.part_cap = 0;
   // item descriptors (4 ints each) after the plan's arrays, one per queue position
-  const int nq = n_queues(g.Hkv);
-  const int64_t per_q_bound = (p.n_tiles * g.Hkv + p.part_cap + nq - 1) / nq;
+  const int64_t per_q_bound = plan_per_q_bound(p.n_tiles, g.Hkv, p.part_cap);
   p.desc_off = (int)((plan_ints(p.n_tiles, max_pieces) + 3) / 4 * 4);
   p.ws_fixed_bytes = ((p.desc_off + 4 * per_q_bound) * sizeof(int) + 255) / 256 * 256;
   p.ws_bytes_per_layer = (size_t)p.part_cap * kQPerWG * (128 * sizeof(uint16_t) + 4 * sizeof(float));
@@ -1324,9 +1425,10 @@ static void launch_mfma_g(const AttnArgs& a, const Rows& rows, const ScatterArgs
   pa.T = a.T;
   pa.RT = kWaves * (32 / G);
   pa.Hkv = a.Hkv;
-  pa.layers = a.layers;
   pa.part_cap = a.part_cap;
   pa.desc_off = a.desc_off;
+  pa.pj_cap = (int)plan_max_pieces(a.T) + 1;
+  pa.desc_cap = (int)(4 * plan_per_q_bound(a.n_tiles, a.Hkv, a.part_cap));
   pa.plan = a.plan;
   if (ra) {
     TraceScope tr("plan_rope_scatter", s);

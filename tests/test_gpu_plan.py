@@ -18,7 +18,7 @@ from tests.test_plan_host import GEOS, check
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
-HDR, SORT_CAP = 16, 2048
+HDR, SORT_CAP, MAGIC = 32, 2048, 0x43530231
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -47,7 +47,8 @@ def test_device_plan_matches_mirror(G, hkv, T, k):
     K, V, Q, KF, VF = z(1, hkv, T, D), z(1, hkv, T, D), z(1, hq, n, D), z(1, hkv, n, D), z(1, hkv, n, D)
     S_dev = torch.from_numpy(sel.astype(np.int32)).cuda()
     out = torch.empty((1, hq, k, D), dtype=torch.bfloat16, device="cuda")
-    ws = torch.empty(b.selective_attend_scatter_workspace(geo, k, 1), dtype=torch.uint8, device="cuda")
+    # (zeroed: a block the allocator hands back may hold a matching plan, which the call would keep)
+    ws = torch.zeros(b.selective_attend_scatter_workspace(geo, k, 1), dtype=torch.uint8, device="cuda")
     b.selective_attend_scatter(geo, K, V, 0, 1, S_dev, k, Q, KF, VF, out, None, ws)
     torch.cuda.synchronize()
     plan = ws.view(torch.int32).cpu().numpy()
@@ -64,6 +65,9 @@ def test_device_plan_matches_mirror(G, hkv, T, k):
     ppre = plan[HDR + 2 * nt:HDR + 3 * nt + 1]
     assert list(nsp) == nsp_w
     assert list(ppre) == want["ppre"]
+    # what the plan was made from (a later call compares it), and a fresh plan's mark
+    assert list(hdr[16:22]) == [MAGIC, nt, 256 // G, hkv, hdr[20], hdr[14]] and hdr[24] == 0
+    assert list(plan[HDR:HDR + nt]) == list(want["nu"])
     # descriptors: {row tile, KV head in the queue | piece << 16, first and end key tile}
     per_q, off = want["per_q"], int(hdr[14])
     d = plan[off:off + 4 * per_q].reshape(per_q, 4)
