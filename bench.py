@@ -263,6 +263,7 @@ def bench_fused_vs_plain(inp, w, rho, steps, binding, torch):
     log(f"[bench] rho={rho}: n_sel={k}, fused RoPE and plain in alternating steps, steps {steps} each")
     times = {False: [], True: []}
     trace = {}  # the fused steps' kernels (both kinds are traced alike: the trace's events cost time)
+    b.cs_trace_only(("sel_attn_mfma", "plan_scatter", "plan_rope_scatter"))
     for i in range(2 * (steps + 1)):
         fused = i % 2 == 1
         inp.K.copy_(inp.K0)
@@ -285,12 +286,19 @@ def bench_fused_vs_plain(inp, w, rho, steps, binding, torch):
                 for name, (n_l, ms) in step_trace.items():
                     n0, ms0 = trace.get(name, (0, 0.0))
                     trace[name] = (n0 + n_l, ms0 + ms)
+    b.cs_trace_only(None)
     fm, pm = float(np.median(times[True])), float(np.median(times[False]))
     log(f"[bench] rho={rho}: fused RoPE compose median {fm:.3f} ms, plain {pm:.3f} ms (alternating steps)")
     return {"ms": fm, "plain_ms": pm, "trace": trace}
 
 
-def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, paged=False, untraced_steps=0):
+# Kernels whose launches the timed steps trace (the two rooflines); every traced launch costs the GPU a few
+# microseconds, so the other kernels' durations come from separate fully traced steps.
+ROOFLINE_KERNELS = ("sel_attn_mfma", "rebase_bf16_d128")
+
+
+def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, paged=False, untraced_steps=0,
+              breakdown_steps=2):
     b = binding
     n = w.n_candidates
     scores = torch.empty(n, dtype=torch.float32, device="cuda")
@@ -326,6 +334,7 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, 
         run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused, paged)
     torch.cuda.synchronize()
     b.cs_trace_reset()
+    b.cs_trace_only(ROOFLINE_KERNELS)
     times = []
     wall0 = time.perf_counter()
     for _ in range(steps):
@@ -343,6 +352,18 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, 
         times.append(e0.elapsed_time(e1))
     wall = time.perf_counter() - wall0
     trace = b.cs_trace_collect()
+    b.cs_trace_only(None)
+    # every kernel's duration, from steps with all launches traced (after the timed ones)
+    b.cs_trace_reset()
+    for _ in range(breakdown_steps):
+        restore()
+        torch.cuda.synchronize()
+        busy_gpu(torch)
+        b.cs_trace_enable(True)
+        run_compose(inp, w, rho, b, torch, out, lse, sel, scores, ws, batched, fused, paged)
+        b.cs_trace_enable(False)
+        torch.cuda.synchronize()
+    breakdown = b.cs_trace_collect() if breakdown_steps else None
     # The same steps without the per-kernel trace, whose events cost the host ~14 us per launch: where
     # a layer call's GPU work is short (the 8k-token cache), the traced steps wait on the host.
     untraced = []
@@ -368,11 +389,17 @@ def bench_rho(inp, w, rho, steps, warmup, binding, torch, batched, fused=False, 
     res = dict(rho=rho, n_sel=k, ms=float(np.median(times)), ms_mean=float(np.mean(times)),
                ms_min=float(np.min(times)), wall_s=wall, steps=steps, trace=trace,
                attn_flops_per_layer=attn_flops_per_layer, rebase_bytes=rebase_bytes, visible=visible,
-               ms_untraced=float(np.median(untraced)) if untraced else None)
+               ms_untraced=float(np.median(untraced)) if untraced else None,
+               breakdown=breakdown, breakdown_steps=breakdown_steps)
     log(f"[bench] rho={rho}: compose median {res['ms']:.3f} ms (min {res['ms_min']:.3f})"
         + (f", untraced {res['ms_untraced']:.3f} ms" if untraced else "") + "; kernels:")
     for name, (cnt, tot) in sorted(trace.items(), key=lambda kv: -kv[1][1]):
         log(f"    {name:24s} launches {cnt:5d}  avg {tot / cnt * 1e3:9.1f} us  total/step {tot / steps:8.3f} ms")
+    if breakdown:
+        log(f"[bench] rho={rho}: every kernel, {breakdown_steps} more steps with all launches traced:")
+        for name, (cnt, tot) in sorted(breakdown.items(), key=lambda kv: -kv[1][1]):
+            log(f"    {name:24s} launches {cnt:5d}  avg {tot / cnt * 1e3:9.1f} us  "
+                f"total/step {tot / breakdown_steps:8.3f} ms")
     return res
 
 
@@ -555,9 +582,11 @@ def sweep_attention(args, b, synth, torch):
                                            inp.VF, out, None, ws)
         stage()  # warm-up
         b.cs_trace_reset()
+        b.cs_trace_only(("sel_attn_mfma",))  # (the other launches untraced: their events cost GPU time)
         b.cs_trace_enable(True)
         med, _ = _events(torch, stream, stage, max(args.steps // 2, 2))
         b.cs_trace_enable(False)
+        b.cs_trace_only(None)
         tr = b.cs_trace_collect()
         an, ams = tr.get("sel_attn_mfma", (1, 0.0))
         kern_tflops = flops / (ams / an * 1e-3) / 1e12
@@ -634,9 +663,12 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=No
     reb_n, reb_ms = tr.get("rebase_bf16_d128", (0, 0.0))
     reb_avg_s = reb_ms / max(reb_n, 1) / 1e3
     reb_gbps = r["rebase_bytes"] / reb_avg_s / 1e9 if reb_n else None
+    # every kernel per step: from the fully traced steps when there are (the timed steps trace the
+    # roofline kernels only)
+    bd, bd_steps = (r["breakdown"], r["breakdown_steps"]) if r.get("breakdown") else (tr, steps)
     # whole attention stage per layer call: scatter (with the plan, in one launch) + attention + combine
-    stage = sum(tr.get(k, (0, 0.0))[1] for k in ("plan_scatter", "scatter_rows", "sel_attn_mfma", "sel_attn_combine"))
-    stage_tflops = w.n_layers * r["attn_flops_per_layer"] / (stage / steps / 1e3) / 1e12 if stage else None
+    stage = sum(bd.get(k, (0, 0.0))[1] for k in ("plan_scatter", "scatter_rows", "sel_attn_mfma", "sel_attn_combine"))
+    stage_tflops = w.n_layers * r["attn_flops_per_layer"] / (stage / bd_steps / 1e3) / 1e12 if stage else None
     line = {
         "metric": "compose ms/65k-token cache; rebase GB/s (% HBM peak); sel-attn TFLOP/s (% MFMA)",
         "value": round(r["ms"], 4),
@@ -659,7 +691,7 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=No
         "sel_attn_TFLOPs": None if attn_tflops is None else round(attn_tflops, 1),
         "sel_attn_frac_mfma": None if attn_tflops is None else round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "sel_attn_stage_TFLOPs": None if stage_tflops is None else round(stage_tflops, 1),
-        "kernels_ms_per_step": {k: round(v[1] / steps, 4) for k, v in tr.items()},
+        "kernels_ms_per_step": {k: round(v[1] / bd_steps, 4) for k, v in bd.items()},
         "roofline": {
             "kernel": "sel_attn_mfma",
             "bound": "mfma",

@@ -363,8 +363,14 @@ const char* cs_last_error(void);
  * lock; a kernel's events reach the collector once its launch is enqueued,
  * so a collect running beside launches on other threads never waits on a
  * half-enqueued pair.  A collect that fails keeps the launches it had not
- * reached. */
+ * reached.
+ *
+ * cs_trace_only(names) narrows tracing to the kernels named in a
+ * comma-separated list (NULL or "": every kernel); the list is copied.  The
+ * events cost the GPU a few microseconds per traced launch, so a caller that
+ * needs one kernel's durations can leave the others untraced. */
 cs_status cs_trace_enable(int32_t on);
+cs_status cs_trace_only(const char* names);
 cs_status cs_trace_collect(void);
 int32_t cs_trace_count(void);
 cs_status cs_trace_get(int32_t i, const char** name, int64_t* launches,

@@ -18,7 +18,8 @@ CS_OK, CS_ERR_INVALID_ARGUMENT, CS_ERR_UNSUPPORTED, CS_ERR_WORKSPACE_TOO_SMALL, 
 CS_F32, CS_BF16 = 0, 1
 EXPORTS = ("compose_rebase_k", "score_deviation_topk_workspace", "score_deviation_topk",
            "selective_attend_scatter_workspace", "selective_attend_scatter", "cs_last_error",
-           "cs_trace_enable", "cs_trace_collect", "cs_trace_count", "cs_trace_get", "cs_trace_reset")
+           "cs_trace_enable", "cs_trace_only", "cs_trace_collect", "cs_trace_count", "cs_trace_get",
+           "cs_trace_reset")
 
 
 class CsError(RuntimeError):
@@ -70,6 +71,7 @@ def lib():
                                                           vp, vp, sz, vp]
         L.cs_last_error.restype = ctypes.c_char_p
         L.cs_trace_enable.argtypes = [i32]
+        L.cs_trace_only.argtypes = [ctypes.c_char_p]
         L.cs_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(i64),
                                    ctypes.POINTER(ctypes.c_double)]
         L.cs_trace_count.restype = i32
@@ -80,7 +82,7 @@ def lib():
                      "selective_attend_scatter_rope_workspace", "selective_attend_scatter_rope",
                      "compose_rebase_k_paged", "compose_rebase_k_tokens_paged", "score_deviation_topk_paged",
                      "selective_attend_scatter_paged", "selective_attend_scatter_rope_paged",
-                     "cs_trace_enable", "cs_trace_collect", "cs_trace_get"):
+                     "cs_trace_enable", "cs_trace_only", "cs_trace_collect", "cs_trace_get"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -193,6 +195,11 @@ def selective_attend_scatter_noalloc(geo, k_cache, v_cache, layer_begin, layer_e
 # ---------------------------------------------------------------- tracing
 def cs_trace_enable(on=True):
     _check(lib().cs_trace_enable(1 if on else 0))
+
+
+def cs_trace_only(names=None):
+    """Trace only the kernels named (an iterable of names, or None for all)."""
+    _check(lib().cs_trace_only(None if names is None else ",".join(names).encode()))
 
 
 def cs_trace_reset():

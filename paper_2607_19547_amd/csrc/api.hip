@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <map>
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -53,6 +54,7 @@ bool g_trace_on = false;
 std::vector<Pending> g_pending;
 std::vector<std::pair<std::string, Acc>> g_acc;
 std::vector<hipEvent_t> g_pool;
+std::vector<std::string> g_trace_names;  // kernels traced while tracing is on (empty: all)
 
 // set while a call that must not allocate enqueues on this thread
 thread_local bool t_trace_suppressed = false;
@@ -74,6 +76,9 @@ TraceScope::TraceScope(const char* n, hipStream_t s) : name(n), stream(s), a(nul
   if (trace_suppressed()) return;
   std::lock_guard<std::mutex> lk(g_trace_mu);
   if (!g_trace_on) return;
+  if (!g_trace_names.empty() &&
+      std::find(g_trace_names.begin(), g_trace_names.end(), n) == g_trace_names.end())
+    return;
   a = take_event();
   b = a ? take_event() : nullptr;
   if (!b) {
@@ -647,6 +652,25 @@ cs_status selective_attend_scatter_rope_paged(const cs_geometry* gp, void* const
 cs_status cs_trace_enable(int32_t on) {
   std::lock_guard<std::mutex> lk(g_trace_mu);
   g_trace_on = on != 0;
+  return CS_OK;
+}
+
+cs_status cs_trace_only(const char* names) {
+  std::vector<std::string> list;
+  if (names) {
+    std::string cur;
+    for (const char* c = names;; ++c) {
+      if (*c == ',' || *c == 0) {
+        if (!cur.empty()) list.push_back(cur);
+        cur.clear();
+        if (*c == 0) break;
+      } else {
+        cur += *c;
+      }
+    }
+  }
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  g_trace_names.swap(list);
   return CS_OK;
 }
 

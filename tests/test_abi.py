@@ -234,3 +234,12 @@ def test_noalloc_attention_argument_errors(built_lib):
     huge = b.Geo(36, 16, 2, 128, (16, 24, 24), "bf16", [0, 64, T])
     code, text = _code(f, huge, FAKE, FAKE, 0, 1, FAKE, 1 << 27, FAKE, FAKE, FAKE, FAKE, stream=0)
     assert code == b.CS_ERR_UNSUPPORTED and "too large" in text
+
+
+def test_trace_filter_without_a_gpu(built_lib):
+    """cs_trace_only only records the names (no device call): it works on a host without a GPU."""
+    from paper_2607_19547_amd import binding as b
+    b.cs_trace_only(["sel_attn_mfma", "rebase_bf16_d128"])
+    b.cs_trace_only([])
+    b.cs_trace_only(None)
+    assert b.cs_trace_collect() == {}
