@@ -68,6 +68,16 @@ def test_device_plan_matches_mirror(G, hkv, T, k):
     # what the plan was made from (a later call compares it), and a fresh plan's mark
     assert list(hdr[16:22]) == [MAGIC, nt, 256 // G, hkv, hdr[20], hdr[14]] and hdr[24] == 0
     assert list(plan[HDR:HDR + nt]) == list(want["nu"])
+    # its checksum: two position-weighted sums (mod 2^32) over the header's [8, 16), pieces and
+    # partial-slot prefixes, piece sections and item descriptors
+    pj0 = HDR + 3 * nt + 1
+    idx = np.concatenate([np.arange(8, 16), np.arange(HDR + nt, pj0), np.arange(pj0, pj0 + nj + 1),
+                          np.arange(int(hdr[14]), int(hdr[14]) + 4 * want["per_q"])]).astype(np.uint64)
+    v = plan.view(np.uint32)[idx.astype(np.int64)].astype(np.uint64)
+    m32 = np.uint64(0xFFFFFFFF)
+    c1 = int(np.sum((v * (2 * idx + 1)) & m32) & m32)
+    c2 = int(np.sum((((v ^ ((idx * 0x9E3779B9) & m32)) * 0x85EBCA6B) & m32) + idx) & m32)
+    assert (c1, c2) == (int(np.uint32(hdr[22])), int(np.uint32(hdr[23]))), "checksum words"
     # descriptors: {row tile, KV head in the queue | piece << 16, first and end key tile}
     per_q, off = want["per_q"], int(hdr[14])
     d = plan[off:off + 4 * per_q].reshape(per_q, 4)
