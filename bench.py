@@ -55,6 +55,9 @@ def parse():
                         "rotated at the global coordinates) and the plain call (0: skip)")
     p.add_argument("--gemm-context", type=int, default=1,
                    help="also time the vendor library's bf16 GEMM on this GPU, as context for the MFMA figure (0: skip)")
+    p.add_argument("--load-steps", type=int, default=3,
+                   help="steps of the chunks' load from page-locked host memory with the re-basing as each "
+                        "chunk lands, against plain copies and copies followed by the re-basing (0: skip)")
     p.add_argument("--paged-steps", type=int, default=3,
                    help="steps also timed on the cache held as one buffer per chunk (0: skip)")
     p.add_argument("--batched-steps", type=int, default=3,
@@ -217,9 +220,55 @@ def main():
     if args.paged_steps > 0:
         paged = bench_rho(inp, w, rho, args.paged_steps, 1, binding, torch, False, paged=True)
     graph = bench_graph(inp, w, rho, args.graph_steps, binding, torch) if args.graph_steps > 0 else None
+    load = bench_load(inp, w, args.load_steps, binding, torch) if args.load_steps > 0 else None
     gemm = gemm_context(torch) if args.gemm_context else None
     cpu = cpu_baseline(w, rho) if args.cpu_baseline else None
-    emit(args, w, rho, result, rho1, cpu, other, fused, paged, gemm, graph)
+    emit(args, w, rho, result, rho1, cpu, other, fused, paged, gemm, graph, load)
+
+
+def bench_load(inp, w, steps, binding, torch):
+    """The cache's chunks (K and V, [L, H_kv, len_c, D] each) from page-locked host memory into device
+    chunk buffers: plain copies; compose_load_rebase_k_paged (copies on a second stream, the keys
+    first, re-based on the compute stream while the values are in transfer); and copies followed by
+    compose_rebase_k_paged.  Medians of HIP events on the compute stream (PCIe included)."""
+    b = binding
+    cs = w.chunk_start
+    n_chunks = len(cs) - 1
+    kh = [inp.K0[:, :, cs[c]:cs[c + 1]].contiguous().cpu().pin_memory() for c in range(n_chunks)]
+    vh = [inp.V0[:, :, cs[c]:cs[c + 1]].contiguous().cpu().pin_memory() for c in range(n_chunks)]
+    kd = [torch.empty_like(x, device="cuda") for x in kh]
+    vd = [torch.empty_like(x, device="cuda") for x in vh]
+    nbytes = sum(x.numel() * x.element_size() for x in kh + vh)
+    stream = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    off = inp.offsets
+
+    def plain():
+        for d, h in zip(kd + vd, kh + vh):
+            d.copy_(h, non_blocking=True)
+
+    def fused():
+        b.compose_load_rebase_k_paged(inp.geo, kd, vd, kh, vh, off, copy_stream=copy.cuda_stream)
+
+    def serial():
+        plain()
+        b.compose_rebase_k_paged(inp.geo, kd, off)
+
+    res = {}
+    for name, fn in (("copy", plain), ("load_rebase", fused), ("copy_then_rebase", serial)):
+        fn()  # (warm)
+        torch.cuda.synchronize()
+        res[name], _ = _events(torch, stream, fn, steps)
+    fused()
+    torch.cuda.synchronize()
+    ref = [x.cuda() for x in kh]
+    b.compose_rebase_k_paged(inp.geo, ref, off)
+    identical = all(torch.equal(x, y) for x, y in zip(kd, ref))
+    log(f"[bench] chunk load from host ({nbytes / 1e9:.2f} GB): copies {res['copy']:.3f} ms "
+        f"({nbytes / res['copy'] / 1e6:.1f} GB/s), with the re-basing during the load {res['load_rebase']:.3f} ms, "
+        f"copies then re-basing {res['copy_then_rebase']:.3f} ms; keys identical to the latter: {identical}")
+    del kh, vh, kd, vd, ref
+    return dict(res, bytes=nbytes, identical=identical)
 
 
 def gemm_context(torch, m=8192, n=8192, k=16384, reps=10):
@@ -654,7 +703,7 @@ def _traffic(kernel):
         return None
 
 
-def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=None, graph=None):
+def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=None, graph=None, load=None):
     tr = r["trace"]
     steps = r["steps"]
     attn_n, attn_ms = tr.get("sel_attn_mfma", (0, 0.0))
@@ -733,6 +782,12 @@ def emit(args, w, rho, r, rho1, cpu, other=None, fused=None, paged=None, gemm=No
         for key, name in (("paged_sel_attn_us", "sel_attn_mfma"), ("paged_rebase_us", "rebase_bf16_d128")):
             if name in pt:
                 line[key] = round(pt[name][1] / pt[name][0] * 1e3, 2)
+    if load is not None:
+        line["chunk_load"] = {"bytes": load["bytes"], "copy_ms": round(load["copy"], 3),
+                              "load_rebase_ms": round(load["load_rebase"], 3),
+                              "copy_then_rebase_ms": round(load["copy_then_rebase"], 3),
+                              "pcie_GBps": round(load["bytes"] / load["load_rebase"] / 1e6, 1),
+                              "identical": load["identical"]}
     if graph is not None:
         line["graph_compose_ms"] = round(graph["ms"], 4)
         line["graph_replays_identical"] = graph["identical"]

@@ -328,6 +328,38 @@ cs_status compose_rebase_k_paged(const cs_geometry* g, void* const* k_chunks,
                                  int32_t* global_coords, void* stream);
 cs_status compose_rebase_k_tokens_paged(const cs_geometry* g, void* const* k_chunks,
                                         const int32_t* token_offsets, void* stream);
+
+/* compose_load_rebase_k_paged -- the chunks' load from host memory with the
+ * re-basing of Eq. 3 done during the load (Section 2: chunks come back from
+ * storage and are re-based before they are concatenated), so that the
+ * rotation hides under the transfer of the values.
+ *
+ * Every chunk's keys are copied from the host to k_chunks[c] on copy_stream,
+ * then every chunk's values to v_chunks[c]; once the keys have landed, stream
+ * re-bases them exactly as compose_rebase_k_paged would (chunks with a zero
+ * offset are copied only) while the values are still in transfer.  The
+ * copies start after the work
+ * enqueued on stream before the call, and when stream reaches the end of the
+ * call's work every copy is complete: the call is one step of stream, and
+ * later work on stream sees the whole composed cache.
+ *   k_host, v_host  HOST arrays of n_chunks HOST pointers, chunk c's keys
+ *                   (values) as [L][H_kv][len_c][D]; page-locked memory
+ *                   (hipHostMalloc) lets the copies overlap the re-basing,
+ *                   pageable memory works but serialises them.  Read before
+ *                   the call's work completes on stream: keep them unchanged
+ *                   until then.
+ *   copy_stream     the stream of the copies; NULL or equal to stream: one
+ *                   stream does everything in order.
+ *   k_chunks, v_chunks, chunk_offsets, stream: as for compose_rebase_k_paged
+ *                   (the destination buffers' prior contents are overwritten).
+ * The results are bit-identical to copying the chunks and then calling
+ * compose_rebase_k_paged.  Errors: those of compose_rebase_k_paged, plus
+ * CS_ERR_INVALID_ARGUMENT for a NULL host array or chunk pointer. */
+cs_status compose_load_rebase_k_paged(const cs_geometry* g, void* const* k_chunks,
+                                      void* const* v_chunks, const void* const* k_host,
+                                      const void* const* v_host,
+                                      const int32_t* chunk_offsets,
+                                      void* copy_stream, void* stream);
 cs_status score_deviation_topk_paged(const cs_geometry* g, void* const* k_chunks,
                                      int32_t score_layer, const void* k_fresh,
                                      double rho, float* scores, int32_t* sel_idx,

@@ -63,6 +63,7 @@ def lib():
         L.selective_attend_scatter_noalloc.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp, vp]
         L.compose_rebase_k_paged.argtypes = [G, vp, vp, vp, vp, vp]
         L.compose_rebase_k_tokens_paged.argtypes = [G, vp, vp, vp]
+        L.compose_load_rebase_k_paged.argtypes = [G, vp, vp, vp, vp, vp, vp, vp]
         L.score_deviation_topk_paged.argtypes = [G, vp, i32, vp, ctypes.c_double, vp, vp,
                                                  ctypes.POINTER(i64), vp, sz, vp]
         L.selective_attend_scatter_paged.argtypes = [G, vp, vp, i32, i32, vp, i64, vp, vp, vp, vp, vp,
@@ -81,6 +82,7 @@ def lib():
                      "selective_attend_scatter_noalloc",
                      "selective_attend_scatter_rope_workspace", "selective_attend_scatter_rope",
                      "compose_rebase_k_paged", "compose_rebase_k_tokens_paged", "score_deviation_topk_paged",
+                     "compose_load_rebase_k_paged",
                      "selective_attend_scatter_paged", "selective_attend_scatter_rope_paged",
                      "cs_trace_enable", "cs_trace_only", "cs_trace_collect", "cs_trace_get"):
             getattr(L, name).restype = ctypes.c_int
@@ -256,6 +258,17 @@ def compose_rebase_k_paged(geo, k_chunks, chunk_offsets, local_coords=None, want
                                         None if glob is None else glob.ctypes.data_as(ctypes.c_void_p),
                                         _stream(stream)))
     return glob
+
+
+def compose_load_rebase_k_paged(geo, k_chunks, v_chunks, k_host, v_host, chunk_offsets, copy_stream=None,
+                                stream=None):
+    """Copy each chunk's K and V from host tensors (page-locked for overlap) into the device chunk
+    tensors on copy_stream, re-basing each chunk's keys on stream as soon as they have landed."""
+    off = np.ascontiguousarray(chunk_offsets, dtype=np.int32)
+    _check(lib().compose_load_rebase_k_paged(geo.ref, _chunks(k_chunks), _chunks(v_chunks), _chunks(k_host),
+                                             _chunks(v_host), off.ctypes.data_as(ctypes.c_void_p),
+                                             None if copy_stream is None else ctypes.c_void_p(copy_stream),
+                                             _stream(stream)))
 
 
 def compose_rebase_k_tokens_paged(geo, k_chunks, token_offsets, stream=None):

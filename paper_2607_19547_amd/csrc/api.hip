@@ -469,6 +469,66 @@ cs_status compose_rebase_k_paged(const cs_geometry* gp, void* const* k_chunks, c
   return rebase_k(gp, g, cv, chunk_offsets, local_coords, global_coords, stream);
 }
 
+// Three events, created on first use and kept: the call's start on the
+// compute stream (the copies wait for the work enqueued before the call), the
+// keys' arrival on the copy stream (the re-basing waits for it) and the last
+// copy (the compute stream waits for it).  A wait takes the event's record at
+// the time it is enqueued, so a later call may record the same events again.
+static std::mutex g_load_mu;
+static hipEvent_t g_load_events[3];
+
+cs_status compose_load_rebase_k_paged(const cs_geometry* gp, void* const* k_chunks, void* const* v_chunks,
+                                      const void* const* k_host, const void* const* v_host,
+                                      const int32_t* chunk_offsets, void* copy_stream, void* stream) {
+  Geo g;
+  cs_status st = check_geometry(gp, &g);
+  if (st) return st;
+  CacheView cv;
+  st = paged_view(g, k_chunks, v_chunks, true, &cv);
+  if (st) return st;
+  if (!k_host || !v_host) return fail(CS_ERR_INVALID_ARGUMENT, "host chunk pointer array is NULL");
+  for (int c = 0; c < g.N; ++c)
+    if (!k_host[c] || !v_host[c])
+      return fail(CS_ERR_INVALID_ARGUMENT, "host chunk " + std::to_string(c) + " is NULL");
+  if (!chunk_offsets) return fail(CS_ERR_INVALID_ARGUMENT, "chunk_offsets is NULL");
+  std::vector<double> theta;
+  st = theta_table(gp, g, &theta);
+  if (!st) st = launch_rebase(g, cv, chunk_offsets, theta.data(), (hipStream_t)stream, true);
+  if (st) return st;
+  const hipStream_t s = (hipStream_t)stream;
+  const hipStream_t cps = copy_stream ? (hipStream_t)copy_stream : s;
+  const bool two = cps != s;
+  std::lock_guard<std::mutex> lk(g_load_mu);  // (the events are shared by every caller)
+  if (two) {
+    for (hipEvent_t& e : g_load_events)
+      if (!e && hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess)
+        return fail(CS_ERR_HIP, "hipEventCreateWithFlags failed");
+    if (hipEventRecord(g_load_events[0], s) != hipSuccess || hipStreamWaitEvent(cps, g_load_events[0], 0) != hipSuccess)
+      return fail(CS_ERR_HIP, "ordering the copies after the stream's earlier work failed");
+  }
+  auto copy = [&](void* const* dst, const void* const* src, const char* what) -> cs_status {
+    for (int c = 0; c < g.N; ++c) {
+      const size_t bytes = (size_t)g.L * g.Hkv * (size_t)(g.cs[c + 1] - g.cs[c]) * g.D * g.esize;
+      if (hipMemcpyAsync(dst[c], src[c], bytes, hipMemcpyHostToDevice, cps) != hipSuccess)
+        return fail(CS_ERR_HIP, "hipMemcpyAsync of chunk " + std::to_string(c) + "'s " + what + " failed");
+    }
+    return CS_OK;
+  };
+  // every chunk's keys, then their re-basing on the compute stream while the
+  // values follow on the copy stream
+  st = copy(k_chunks, k_host, "keys");
+  if (st) return st;
+  if (two && (hipEventRecord(g_load_events[1], cps) != hipSuccess || hipStreamWaitEvent(s, g_load_events[1], 0) != hipSuccess))
+    return fail(CS_ERR_HIP, "ordering the re-basing after the keys' copies failed");
+  st = launch_rebase(g, cv, chunk_offsets, theta.data(), s);
+  if (st) return st;
+  st = copy(v_chunks, v_host, "values");
+  if (st) return st;
+  if (two && (hipEventRecord(g_load_events[2], cps) != hipSuccess || hipStreamWaitEvent(s, g_load_events[2], 0) != hipSuccess))
+    return fail(CS_ERR_HIP, "ordering the stream after the last copy failed");
+  return check_launch("load and re-base");
+}
+
 cs_status compose_rebase_k_tokens(const cs_geometry* gp, void* k_cache, const int32_t* token_offsets,
                                   void* stream) {
   Geo g;

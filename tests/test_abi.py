@@ -183,6 +183,14 @@ def test_paged_argument_errors(built_lib):
                  FAKE, FAKE, stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
     # nothing to do: OK without looking at the chunk arrays
     b.selective_attend_scatter_paged(g, None, None, 0, 1, None, 0, None, None, None, None, stream=0)
+    # load and re-base: device and host chunk arrays, each with every chunk
+    off = np.zeros((2, 3))
+    assert _code(b.compose_load_rebase_k_paged, g, chunks, None, chunks, chunks, off,
+                 stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
+    code, text = _code(b.compose_load_rebase_k_paged, g, chunks, chunks, [FAKE, None], chunks, off, stream=0)
+    assert code == b.CS_ERR_INVALID_ARGUMENT and "host chunk 1" in text
+    assert _code(b.compose_load_rebase_k_paged, g, chunks, chunks, chunks, None, off,
+                 stream=0)[0] == b.CS_ERR_INVALID_ARGUMENT
 
 
 def test_paged_limits(built_lib):
