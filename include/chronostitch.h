@@ -21,7 +21,9 @@
  *    grid limits (caches of tens of millions of tokens per call): every launch
  *    of the call is sized first, and such a call returns CS_ERR_UNSUPPORTED.
  *  - DEVICE pointers are device memory of the current HIP device; HOST
- *    pointers are read (or written) before the call returns.  The caller
+ *    pointers are read (or written) before the call returns, except the host
+ *    chunk data of compose_load_rebase_k_paged, which its enqueued copies
+ *    read (the pointer arrays themselves are read before it returns).  The caller
  *    owns every buffer; the library allocates no device memory.  Scratch
  *    memory is a caller-provided workspace sized by the *_workspace query.
  *  - Device work is asynchronous on `stream` (a hipStream_t; NULL = the null
