@@ -203,3 +203,26 @@ def test_fused_rope_calls_reuse_the_plan():
             outs.append(out[layer])
         assert torch.equal(outs[0], outs[1]), f"layer {layer}"
     assert torch.equal(K, K2) and torch.equal(V, V2)
+
+
+def test_batched_call_keeps_the_per_layer_plan():
+    """A call over all layers finds the plan the per-layer calls left (the plan
+    does not depend on the layer count) and gives the outputs of a batched call
+    with a fresh workspace."""
+    b = B()
+    c = Case(20000, 2500, seed=29)
+    log("case plan reuse: a batched call after per-layer calls")
+    nbytes = b.selective_attend_scatter_workspace(c.geo, c.k, c.L)
+    ws = torch.randint(0, 256, (nbytes,), dtype=torch.uint8, device="cuda")
+    K, V = c.K0.clone(), c.V0.clone()
+    for layer in range(c.L):
+        c.call(K, V, layer, c.sel, ws)
+    outs = []
+    for w, want in ((ws, 1), (torch.randint(0, 256, (nbytes,), dtype=torch.uint8, device="cuda"), 0)):
+        out, lse = c.outputs()
+        b.selective_attend_scatter(c.geo, c.K0.clone(), c.V0.clone(), 0, c.L, c.sel, c.k, c.Q, c.KF, c.VF, out, lse,
+                                   w)
+        torch.cuda.synchronize()
+        assert reused(w) == want
+        outs.append((out, lse))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
